@@ -1,0 +1,59 @@
+// Device-side helpers shared by the gfx950 kernels of the DiT step.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace ditmi {
+
+typedef uint16_t bf16_t;  // storage type of bfloat16 in memory
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2v __attribute__((ext_vector_type(2)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ float bf2f(bf16_t v) { return __uint_as_float(((uint32_t)v) << 16); }
+
+// Round-to-nearest-even float -> bf16 pair packed in one dword (low = a).
+__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
+  bf16x2v v = {(__bf16)a, (__bf16)b};
+  return __builtin_bit_cast(uint32_t, v);
+}
+__device__ __forceinline__ bf16_t f2bf(float a) {
+  __bf16 v = (__bf16)a;
+  return __builtin_bit_cast(bf16_t, v);
+}
+
+template <typename T> __device__ __forceinline__ float ld_as_float(const T* p, long i);
+template <> __device__ __forceinline__ float ld_as_float<float>(const float* p, long i) { return p[i]; }
+template <> __device__ __forceinline__ float ld_as_float<bf16_t>(const bf16_t* p, long i) { return bf2f(p[i]); }
+
+__device__ __forceinline__ float warp_sum(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+// Value held by lane (l ^ 32): the other half of a 64-wide wavefront.
+__device__ __forceinline__ float other_half(float v) { return __shfl_xor(v, 32, 64); }
+
+// tanh-approximated GELU; tanh(z) = 1 - 2 / (exp(2z) + 1).
+__device__ __forceinline__ float gelu_tanh(float u) {
+  const float k0 = 0.7978845608028654f;  // sqrt(2/pi)
+  float z = k0 * (u + 0.044715f * u * u * u);
+  float t = 1.0f - 2.0f / (__expf(2.0f * z) + 1.0f);
+  return 0.5f * u * (1.0f + t);
+}
+
+__device__ __forceinline__ float silu(float z) { return z / (1.0f + __expf(-z)); }
+
+// Workgroup id -> logical tile id so that consecutive logical tiles land on
+// the same XCD (workgroups are dispatched round-robin over the 8 XCDs).
+__device__ __forceinline__ int xcd_remap(int i, int n) {
+  const int X = 8;
+  int q = n / X, r = n % X;
+  int xcd = i % X, idx = i / X;
+  return xcd < r ? xcd * (q + 1) + idx : r * (q + 1) + (xcd - r) * q + idx;
+}
+
+}  // namespace ditmi

@@ -1,0 +1,613 @@
+// Host side of the DiT-step library: C ABI, argument validation, workspace
+// layout, GEMM tile planning and the launch sequence of a block and a step.
+// Every argument is checked before the first launch, so a failing call
+// enqueues nothing.  The library allocates no device memory: all tensors and
+// the workspace belong to the caller.
+#include <hip/hip_runtime.h>
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "ditmi.h"
+#include "kernels.h"
+
+using namespace ditmi;
+
+namespace {
+
+thread_local std::string g_err;
+
+dit_status fail(dit_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return st;
+}
+
+inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+inline bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
+inline long rup(long x, long m) { return (x + m - 1) / m * m; }
+
+// ------------------------------------------------------------------ validation
+dit_status check_shape(const dit_shape* s, bool step) {
+  if (!s) return fail(DIT_ERR_INVALID_ARG, "shape is NULL");
+  if (s->batch < 1 || s->tokens < 1 || s->text_tokens < 0)
+    return fail(DIT_ERR_INVALID_ARG, "batch (%d) and tokens (%d) must be >= 1, text_tokens (%d) >= 0", s->batch,
+                s->tokens, s->text_tokens);
+  if (s->hidden < 64 || s->hidden % 64 != 0)
+    return fail(DIT_ERR_INVALID_ARG, "hidden (%d) must be a positive multiple of 64", s->hidden);
+  if (s->hidden > 4096) return fail(DIT_ERR_UNSUPPORTED, "hidden %d > 4096 is not supported", s->hidden);
+  if (s->heads < 1 || s->head_dim < 1) return fail(DIT_ERR_INVALID_ARG, "heads and head_dim must be >= 1");
+  if ((long)s->heads * s->head_dim != s->hidden)
+    return fail(DIT_ERR_INVALID_ARG, "heads*head_dim (%d*%d) != hidden (%d)", s->heads, s->head_dim, s->hidden);
+  if (s->head_dim != 64 && s->head_dim != 72 && s->head_dim != 128)
+    return fail(DIT_ERR_UNSUPPORTED, "head_dim %d not supported (64, 72, 128)", s->head_dim);
+  if (s->mlp_hidden < 64 || s->mlp_hidden % 64 != 0)
+    return fail(DIT_ERR_INVALID_ARG, "mlp_hidden (%d) must be a positive multiple of 64", s->mlp_hidden);
+  if (s->dtype != DIT_F32 && s->dtype != DIT_BF16) return fail(DIT_ERR_INVALID_ARG, "dtype %d unknown", s->dtype);
+  if (!(s->ln_eps > 0.f) || !isfinite(s->ln_eps)) return fail(DIT_ERR_INVALID_ARG, "ln_eps must be finite and > 0");
+  const long rows = (long)s->batch * (s->tokens + s->text_tokens);
+  const long widest = s->mlp_hidden > 3 * s->hidden ? s->mlp_hidden : 3L * s->hidden;
+  if (rows * widest >= (1L << 31) || rows >= (1L << 24))
+    return fail(DIT_ERR_UNSUPPORTED, "batch*tokens (%ld rows) too large", rows);
+  if (step) {
+    if (s->n_blocks < 1) return fail(DIT_ERR_INVALID_ARG, "n_blocks (%d) must be >= 1", s->n_blocks);
+    if (s->patch_in < 1 || s->patch_in > 256 || s->patch_out < 1 || s->patch_out > 256)
+      return fail(DIT_ERR_INVALID_ARG, "patch_in (%d) and patch_out (%d) must be in [1, 256]", s->patch_in,
+                  s->patch_out);
+  }
+  return DIT_OK;
+}
+
+struct Layout {
+  size_t mod, h, q, k, v, o, g, x, feat, h1, total;
+  int ns, Tj, Tj_pad;
+};
+
+Layout layout(const dit_shape* s, int kind) {
+  Layout L{};
+  const size_t E = s->dtype == DIT_BF16 ? 2 : 4;
+  const size_t B = s->batch, T = s->tokens, Tt = s->text_tokens, D = s->hidden, F = s->mlp_hidden;
+  const size_t H = s->heads, dh = s->head_dim;
+  L.ns = Tt > 0 ? 2 : 1;
+  L.Tj = (int)(T + Tt);
+  L.Tj_pad = (int)rup(L.Tj, 8);
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    size_t o = off;
+    off += align256(bytes);
+    return o;
+  };
+  if (kind == DIT_WS_COND) {
+    L.feat = take(B * 256 * 4);
+    L.h1 = take(B * D * 4);
+    L.total = off;
+    return L;
+  }
+  const size_t rows = B * (T + Tt);
+  const size_t nmod = kind == DIT_WS_STEP ? (size_t)s->n_blocks * L.ns * B * 6 * D + B * 2 * D : L.ns * B * 6 * D;
+  L.mod = take(nmod * 4);
+  L.h = take(rows * D * E);
+  L.q = take(B * H * L.Tj * dh * E);
+  L.k = take(B * H * L.Tj * dh * E);
+  L.v = take(E == 2 ? B * H * dh * (size_t)L.Tj_pad * 2 : B * H * L.Tj * dh * 4);
+  L.o = take(rows * D * E);
+  L.g = take(rows * F * E);
+  L.x = kind == DIT_WS_STEP ? take(B * T * D * 4) : 0;
+  L.total = off;
+  return L;
+}
+
+dit_status check_stream_weights(const dit_stream_weights& w, const char* which) {
+  const void* mats[] = {w.w_ada, w.w_qkv, w.w_o, w.w_fc1, w.w_fc2};
+  const void* vecs[] = {w.b_ada, w.b_qkv, w.b_o, w.b_fc1, w.b_fc2};
+  for (const void* p : mats)
+    if (!p || !aligned(p, 16)) return fail(DIT_ERR_INVALID_ARG, "%s weight matrix NULL or not 16-byte aligned", which);
+  for (const void* p : vecs)
+    if (!p || !aligned(p, 4)) return fail(DIT_ERR_INVALID_ARG, "%s bias NULL or misaligned", which);
+  return DIT_OK;
+}
+
+// ------------------------------------------------------------------ timing hook
+struct Timing {
+  std::mutex mu;
+  int kclass = -1, max = 0, used = 0;
+  std::vector<hipEvent_t> ev;
+  double flops = 0, bytes = 0;
+} g_timing;
+
+template <typename Fn>
+hipError_t timed(int kclass, double flops, double bytes, hipStream_t st, Fn&& launch) {
+  bool rec = false;
+  int slot = 0;
+  {
+    std::lock_guard<std::mutex> lk(g_timing.mu);
+    if (g_timing.kclass == kclass && g_timing.used < g_timing.max) {
+      rec = true;
+      slot = g_timing.used++;
+      g_timing.flops += flops;
+      g_timing.bytes += bytes;
+    }
+  }
+  if (rec) {
+    hipError_t e = hipEventRecord(g_timing.ev[2 * slot], st);
+    if (e != hipSuccess) return e;
+  }
+  hipError_t e = launch();
+  if (e != hipSuccess) return e;
+  if (rec) return hipEventRecord(g_timing.ev[2 * slot + 1], st);
+  return hipSuccess;
+}
+
+// ------------------------------------------------------------------ GEMM planning
+struct Gemm {
+  GemmArgs a{};
+  int epi = EPI_STORE;
+  int kclass = DIT_K_OTHER;
+  double flops = 0, bytes = 0;
+};
+
+// Pick the bf16 tile shape that minimises (waves of 256 tiles) x (tile work /
+// tile efficiency); larger tiles reuse more operand bytes per MFMA.
+int choose_tile(const GemmProb* p, int np) {
+  static const double eff[TILE_COUNT] = {1.0, 0.82, 0.82, 0.62};
+  int best = TILE_128x128;
+  double best_cost = 1e300;
+  for (int t = 0; t < TILE_COUNT; ++t) {
+    int bm, bn;
+    gemm_tile_dims(t, &bm, &bn);
+    long tiles = 0;
+    for (int i = 0; i < np; ++i) tiles += (long)((p[i].M + bm - 1) / bm) * ((p[i].N + bn - 1) / bn);
+    const double waves = (double)((tiles + 255) / 256);
+    const double cost = waves * bm * bn / eff[t];
+    if (cost < best_cost - 1e-9) {
+      best_cost = cost;
+      best = t;
+    }
+  }
+  return best;
+}
+
+hipError_t run_gemm(Gemm& G, int dtype, hipStream_t st) {
+  GemmArgs& a = G.a;
+  int bm = 64, bn = 64, tcfg = 0;
+  if (dtype == DIT_BF16) {
+    tcfg = choose_tile(a.p, a.nprob);
+    gemm_tile_dims(tcfg, &bm, &bn);
+  }
+  int tiles = 0;
+  for (int i = 0; i < a.nprob; ++i) {
+    GemmProb& p = a.p[i];
+    p.tiles_m = (p.M + bm - 1) / bm;
+    p.tiles_n = (p.N + bn - 1) / bn;
+    p.tile_begin = tiles;
+    tiles += p.tiles_m * p.tiles_n;
+  }
+  a.total_tiles = tiles;
+  if (tiles == 0) return hipSuccess;
+  return timed(G.kclass, G.flops, G.bytes, st, [&]() {
+    return dtype == DIT_BF16 ? launch_gemm_bf16(a, G.epi, tcfg, st) : launch_gemm_f32(a, G.epi, st);
+  });
+}
+
+// ------------------------------------------------------------------ block sequence
+struct StreamIO {
+  const dit_stream_weights* w;
+  float* x;           // residual [B, Ts, D]
+  const float* mod;   // [B, 6D]
+  int Ts;             // tokens of this stream per sample
+};
+
+#define HIP_TRY(expr)                                                                     \
+  do {                                                                                    \
+    hipError_t _e = (expr);                                                               \
+    if (_e != hipSuccess) return fail(DIT_ERR_HIP, "%s: %s", #expr, hipGetErrorString(_e)); \
+  } while (0)
+
+dit_status run_block(const dit_shape* s, const Layout& L, char* ws, StreamIO* io, int ns, hipStream_t st) {
+  const int B = s->batch, D = s->hidden, F = s->mlp_hidden, H = s->heads, dh = s->head_dim;
+  const int dt = s->dtype;
+  const size_t E = dt == DIT_BF16 ? 2 : 4;
+  char* h = ws + L.h;
+  char* o = ws + L.o;
+  char* gbuf = ws + L.g;
+  const long rows0 = (long)B * io[0].Ts;
+  // row offsets of stream 1 inside the stream-major activation buffers
+  auto act = [&](char* base, int si, long width) { return (void*)(base + (si ? rows0 * width * E : 0)); };
+
+  auto ln = [&](int which) -> hipError_t {  // which 0: (shift1, scale1), 1: (shift2, scale2)
+    LnArgs a{};
+    a.nseg = ns;
+    a.D = D;
+    a.eps = s->ln_eps;
+    long begin = 0;
+    for (int i = 0; i < ns; ++i) {
+      LnSeg& g = a.s[i];
+      g.x = io[i].x;
+      g.out = act(h, i, D);
+      g.shift = io[i].mod + (which ? 3 : 0) * D;
+      g.scale = io[i].mod + (which ? 4 : 1) * D;
+      g.rows = B * io[i].Ts;
+      g.rows_per_batch = io[i].Ts;
+      g.mod_stride = 6 * D;
+      g.row_begin = (int)begin;
+      begin += g.rows;
+    }
+    a.total_rows = (int)begin;
+    const double bytes = (double)begin * D * (4 + E);
+    return timed(DIT_K_LN_MOD, 0, bytes, st, [&]() { return launch_ln_mod(a, dt, st); });
+  };
+  auto prob_common = [&](GemmProb& p, int i, const void* A, const void* W, const void* bias, int N, int K) {
+    p.A = A;
+    p.W = W;
+    p.bias = bias;
+    p.M = B * io[i].Ts;
+    p.N = N;
+    p.K = K;
+    p.rows_per_batch = io[i].Ts;
+  };
+  double tokens = 0;
+  for (int i = 0; i < ns; ++i) tokens += (double)B * io[i].Ts;
+
+  // (1) h = LN(x) * (1 + scale1) + shift1
+  HIP_TRY(ln(0));
+  // (2) q, k, v = h W_qkv^T + b_qkv, scattered head-major
+  {
+    Gemm G;
+    G.epi = EPI_QKV;
+    G.kclass = DIT_K_GEMM_QKV;
+    G.a.nprob = ns;
+    for (int i = 0; i < ns; ++i) {
+      GemmProb& p = G.a.p[i];
+      prob_common(p, i, act(h, i, D), io[i].w->w_qkv, io[i].w->b_qkv, 3 * D, D);
+      p.q = ws + L.q;
+      p.k = ws + L.k;
+      p.v = ws + L.v;
+      p.seq_off = i ? io[0].Ts : 0;
+      p.Tj = L.Tj;
+      p.Tj_pad = L.Tj_pad;
+      p.heads = H;
+      p.head_dim = dh;
+      p.hidden = D;
+    }
+    G.flops = 2.0 * tokens * 3 * D * D;
+    G.bytes = (tokens * D + ns * 3.0 * D * D + tokens * 3 * D) * E;
+    HIP_TRY(run_gemm(G, dt, st));
+  }
+  // (3) o = softmax(q k^T / sqrt(dh)) v over the joint sequence
+  {
+    AttnArgs a{};
+    a.q = ws + L.q;
+    a.k = ws + L.k;
+    a.v = ws + L.v;
+    a.o = o;
+    a.B = B;
+    a.H = H;
+    a.Tj = L.Tj;
+    a.Tj_pad = L.Tj_pad;
+    a.T_img = io[0].Ts;
+    a.T_txt = ns > 1 ? io[1].Ts : 0;
+    a.D = D;
+    a.scale = 1.0f / sqrtf((float)dh);
+    a.scale_log2 = (float)(1.4426950408889634 / sqrt((double)dh));
+    const double flops = 4.0 * B * H * (double)L.Tj * L.Tj * dh;
+    const double bytes = 4.0 * B * (double)L.Tj * D * E;
+    HIP_TRY(timed(DIT_K_ATTENTION, flops, bytes, st, [&]() {
+      return dt == DIT_BF16 ? launch_attn_bf16(a, dh, st) : launch_attn_f32(a, dh, st);
+    }));
+  }
+  // (4) x += gate1 * (o W_o^T + b_o)
+  {
+    Gemm G;
+    G.epi = EPI_RESID;
+    G.kclass = DIT_K_GEMM_OUT;
+    G.a.nprob = ns;
+    for (int i = 0; i < ns; ++i) {
+      GemmProb& p = G.a.p[i];
+      prob_common(p, i, act(o, i, D), io[i].w->w_o, io[i].w->b_o, D, D);
+      p.resid = io[i].x;
+      p.gate = io[i].mod + 2 * D;
+      p.gate_stride = 6 * D;
+    }
+    G.flops = 2.0 * tokens * D * D;
+    G.bytes = (tokens * D + ns * (double)D * D) * E + tokens * D * 8.0;
+    HIP_TRY(run_gemm(G, dt, st));
+  }
+  // (5) h = LN(x) * (1 + scale2) + shift2
+  HIP_TRY(ln(1));
+  // (6) g = GELU(h W_1^T + b_1)
+  {
+    Gemm G;
+    G.epi = EPI_GELU;
+    G.kclass = DIT_K_GEMM_FC1;
+    G.a.nprob = ns;
+    for (int i = 0; i < ns; ++i) {
+      GemmProb& p = G.a.p[i];
+      prob_common(p, i, act(h, i, D), io[i].w->w_fc1, io[i].w->b_fc1, F, D);
+      p.out = act(gbuf, i, F);
+    }
+    G.flops = 2.0 * tokens * F * D;
+    G.bytes = (tokens * D + ns * (double)F * D + tokens * F) * E;
+    HIP_TRY(run_gemm(G, dt, st));
+  }
+  // (7) x += gate2 * (g W_2^T + b_2)
+  {
+    Gemm G;
+    G.epi = EPI_RESID;
+    G.kclass = DIT_K_GEMM_FC2;
+    G.a.nprob = ns;
+    for (int i = 0; i < ns; ++i) {
+      GemmProb& p = G.a.p[i];
+      prob_common(p, i, act(gbuf, i, F), io[i].w->w_fc2, io[i].w->b_fc2, D, F);
+      p.resid = io[i].x;
+      p.gate = io[i].mod + 5 * D;
+      p.gate_stride = 6 * D;
+    }
+    G.flops = 2.0 * tokens * D * F;
+    G.bytes = (tokens * F + ns * (double)D * F) * E + tokens * D * 8.0;
+    HIP_TRY(run_gemm(G, dt, st));
+  }
+  return DIT_OK;
+}
+
+// adaLN GEMVs for a list of (W, bias, out, N) in launches of <= 64 entries.
+struct AdaJob {
+  const void* W;
+  const void* bias;
+  float* out;
+  int N;
+};
+
+dit_status run_adaln(const dit_shape* s, const float* cond, const std::vector<AdaJob>& jobs, hipStream_t st) {
+  const size_t E = s->dtype == DIT_BF16 ? 2 : 4;
+  for (size_t j0 = 0; j0 < jobs.size(); j0 += ADA_MAX_ENTRIES) {
+    AdaArgs a{};
+    a.cond = cond;
+    a.B = s->batch;
+    a.D = s->hidden;
+    int wg = 0;
+    double bytes = 0;
+    const size_t j1 = j0 + ADA_MAX_ENTRIES < jobs.size() ? j0 + ADA_MAX_ENTRIES : jobs.size();
+    for (size_t j = j0; j < j1; ++j) {
+      AdaEntry& e = a.e[a.ne++];
+      e.W = jobs[j].W;
+      e.bias = jobs[j].bias;
+      e.out = jobs[j].out;
+      e.N = jobs[j].N;
+      e.wg_begin = wg;
+      wg += (jobs[j].N + 127) / 128;
+      bytes += (double)jobs[j].N * s->hidden * E;
+    }
+    a.total_wg = wg;
+    HIP_TRY(timed(DIT_K_ADALN, 2.0 * bytes / E * s->batch, bytes, st,
+                  [&]() { return launch_adaln(a, s->dtype, st); }));
+  }
+  return DIT_OK;
+}
+
+}  // namespace
+
+// ====================================================================== C ABI
+extern "C" {
+
+int dit_version(void) { return DITMI_VERSION; }
+
+const char* dit_status_string(dit_status st) {
+  switch (st) {
+    case DIT_OK: return "ok";
+    case DIT_ERR_INVALID_ARG: return "invalid argument";
+    case DIT_ERR_UNSUPPORTED: return "unsupported shape";
+    case DIT_ERR_WORKSPACE: return "workspace too small";
+    case DIT_ERR_HIP: return "HIP runtime error";
+  }
+  return "unknown status";
+}
+
+const char* dit_last_error(void) { return g_err.c_str(); }
+
+size_t dit_workspace_bytes(const dit_shape* s, int kind) {
+  if (kind != DIT_WS_BLOCK && kind != DIT_WS_STEP && kind != DIT_WS_COND) {
+    fail(DIT_ERR_INVALID_ARG, "unknown workspace kind %d", kind);
+    return 0;
+  }
+  if (check_shape(s, kind == DIT_WS_STEP) != DIT_OK) return 0;
+  return layout(s, kind).total;
+}
+
+dit_status dit_block_forward(const dit_shape* s, const dit_block_weights* w, float* x, float* x_txt,
+                             const float* cond, void* workspace, size_t ws_bytes, void* stream) {
+  dit_status st = check_shape(s, false);
+  if (st != DIT_OK) return st;
+  if (!w) return fail(DIT_ERR_INVALID_ARG, "weights is NULL");
+  if ((st = check_stream_weights(w->img, "image-stream")) != DIT_OK) return st;
+  const bool joint = s->text_tokens > 0;
+  if (joint && (st = check_stream_weights(w->txt, "text-stream")) != DIT_OK) return st;
+  if (!x || !aligned(x, 16)) return fail(DIT_ERR_INVALID_ARG, "x NULL or not 16-byte aligned");
+  if (joint && (!x_txt || !aligned(x_txt, 16))) return fail(DIT_ERR_INVALID_ARG, "x_txt NULL or not 16-byte aligned");
+  if (!joint && x_txt) return fail(DIT_ERR_INVALID_ARG, "x_txt must be NULL when text_tokens == 0");
+  if (!cond || !aligned(cond, 4)) return fail(DIT_ERR_INVALID_ARG, "cond NULL or misaligned");
+  const Layout L = layout(s, DIT_WS_BLOCK);
+  if (!workspace || !aligned(workspace, 256)) return fail(DIT_ERR_INVALID_ARG, "workspace NULL or not 256-byte aligned");
+  if (ws_bytes < L.total) return fail(DIT_ERR_WORKSPACE, "workspace %zu bytes < %zu needed", ws_bytes, L.total);
+
+  hipStream_t hs = (hipStream_t)stream;
+  char* ws = (char*)workspace;
+  float* mod = (float*)(ws + L.mod);
+  const size_t per = (size_t)s->batch * 6 * s->hidden;
+  std::vector<AdaJob> jobs;
+  jobs.push_back({w->img.w_ada, w->img.b_ada, mod, 6 * s->hidden});
+  if (joint) jobs.push_back({w->txt.w_ada, w->txt.b_ada, mod + per, 6 * s->hidden});
+  if ((st = run_adaln(s, cond, jobs, hs)) != DIT_OK) return st;
+  StreamIO io[2] = {{&w->img, x, mod, s->tokens}, {&w->txt, x_txt, mod + per, s->text_tokens}};
+  return run_block(s, L, ws, io, joint ? 2 : 1, hs);
+}
+
+dit_status dit_step_forward(const dit_shape* s, const dit_step_weights* w, const float* patches, float* x_txt,
+                            const float* cond, float* out, void* workspace, size_t ws_bytes, void* stream) {
+  dit_status st = check_shape(s, true);
+  if (st != DIT_OK) return st;
+  if (!w || !w->blocks) return fail(DIT_ERR_INVALID_ARG, "step weights or block array is NULL");
+  if (!w->w_patch || !w->b_patch || !w->w_ada_final || !w->b_ada_final || !w->w_final || !w->b_final)
+    return fail(DIT_ERR_INVALID_ARG, "a step weight pointer is NULL");
+  if (!aligned(w->w_ada_final, 16) || !aligned(w->w_final, 16) || !aligned(w->w_patch, 4))
+    return fail(DIT_ERR_INVALID_ARG, "step weight matrix misaligned");
+  if (w->pos && !aligned(w->pos, 4)) return fail(DIT_ERR_INVALID_ARG, "pos misaligned");
+  const bool joint = s->text_tokens > 0;
+  for (int l = 0; l < s->n_blocks; ++l) {
+    if ((st = check_stream_weights(w->blocks[l].img, "image-stream")) != DIT_OK) return st;
+    if (joint && (st = check_stream_weights(w->blocks[l].txt, "text-stream")) != DIT_OK) return st;
+  }
+  if (!patches || !aligned(patches, 4)) return fail(DIT_ERR_INVALID_ARG, "patches NULL or misaligned");
+  if (joint && (!x_txt || !aligned(x_txt, 16))) return fail(DIT_ERR_INVALID_ARG, "x_txt NULL or not 16-byte aligned");
+  if (!joint && x_txt) return fail(DIT_ERR_INVALID_ARG, "x_txt must be NULL when text_tokens == 0");
+  if (!cond || !aligned(cond, 4)) return fail(DIT_ERR_INVALID_ARG, "cond NULL or misaligned");
+  if (!out || !aligned(out, 4)) return fail(DIT_ERR_INVALID_ARG, "out NULL or misaligned");
+  const Layout L = layout(s, DIT_WS_STEP);
+  if (!workspace || !aligned(workspace, 256)) return fail(DIT_ERR_INVALID_ARG, "workspace NULL or not 256-byte aligned");
+  if (ws_bytes < L.total) return fail(DIT_ERR_WORKSPACE, "workspace %zu bytes < %zu needed", ws_bytes, L.total);
+
+  hipStream_t hs = (hipStream_t)stream;
+  char* ws = (char*)workspace;
+  const int B = s->batch, T = s->tokens, D = s->hidden, ns = L.ns;
+  float* mod = (float*)(ws + L.mod);
+  const size_t per = (size_t)B * 6 * D;
+  float* mod_final = mod + (size_t)s->n_blocks * ns * per;
+  float* x = (float*)(ws + L.x);
+
+  // (a2) every block's modulation vectors and the final layer's, hoisted
+  std::vector<AdaJob> jobs;
+  for (int l = 0; l < s->n_blocks; ++l) {
+    jobs.push_back({w->blocks[l].img.w_ada, w->blocks[l].img.b_ada, mod + (size_t)(l * ns) * per, 6 * D});
+    if (joint) jobs.push_back({w->blocks[l].txt.w_ada, w->blocks[l].txt.b_ada, mod + (size_t)(l * ns + 1) * per, 6 * D});
+  }
+  jobs.push_back({w->w_ada_final, w->b_ada_final, mod_final, 2 * D});
+  if ((st = run_adaln(s, cond, jobs, hs)) != DIT_OK) return st;
+
+  // (a3) x = patches W_patch^T + b_patch (+ pos)
+  HIP_TRY(timed(DIT_K_OTHER, 2.0 * B * T * D * s->patch_in, (double)B * T * (s->patch_in + D) * 4.0, hs, [&]() {
+    return launch_patch_embed(B * T, T, s->patch_in, D, patches, w->w_patch, w->b_patch, w->pos, x, s->dtype, hs);
+  }));
+
+  // (a4-a11) blocks
+  for (int l = 0; l < s->n_blocks; ++l) {
+    StreamIO io[2] = {{&w->blocks[l].img, x, mod + (size_t)(l * ns) * per, T},
+                      {&w->blocks[l].txt, x_txt, mod + (size_t)(l * ns + 1) * per, s->text_tokens}};
+    if ((st = run_block(s, L, ws, io, ns, hs)) != DIT_OK) return st;
+  }
+
+  // (a12) out = (LN(x) * (1 + scale_f) + shift_f) W_final^T + b_final, image tokens only
+  {
+    LnArgs a{};
+    a.nseg = 1;
+    a.D = D;
+    a.eps = s->ln_eps;
+    a.total_rows = B * T;
+    a.s[0] = LnSeg{x, ws + L.h, mod_final, mod_final + D, B * T, T, 2 * D, 0};
+    HIP_TRY(timed(DIT_K_LN_MOD, 0, (double)B * T * D * 6.0, hs, [&]() { return launch_ln_mod(a, s->dtype, hs); }));
+    Gemm G;
+    G.epi = EPI_STORE;
+    G.kclass = DIT_K_OTHER;
+    G.a.nprob = 1;
+    GemmProb& p = G.a.p[0];
+    p.A = ws + L.h;
+    p.W = w->w_final;
+    p.bias = w->b_final;
+    p.M = B * T;
+    p.N = s->patch_out;
+    p.K = D;
+    p.rows_per_batch = T;
+    p.out = out;
+    G.flops = 2.0 * B * T * D * s->patch_out;
+    HIP_TRY(run_gemm(G, s->dtype, hs));
+  }
+  return DIT_OK;
+}
+
+dit_status dit_cond_embed(const dit_shape* s, const float* t, const int32_t* y, const void* w_t1, const void* b_t1,
+                          const void* w_t2, const void* b_t2, const void* class_table, float* cond, void* workspace,
+                          size_t ws_bytes, void* stream) {
+  dit_status st = check_shape(s, false);
+  if (st != DIT_OK) return st;
+  if (!t || !y || !w_t1 || !b_t1 || !w_t2 || !b_t2 || !class_table || !cond)
+    return fail(DIT_ERR_INVALID_ARG, "a conditioning pointer is NULL");
+  const Layout L = layout(s, DIT_WS_COND);
+  if (!workspace || !aligned(workspace, 256)) return fail(DIT_ERR_INVALID_ARG, "workspace NULL or not 256-byte aligned");
+  if (ws_bytes < L.total) return fail(DIT_ERR_WORKSPACE, "workspace %zu bytes < %zu needed", ws_bytes, L.total);
+  hipStream_t hs = (hipStream_t)stream;
+  char* ws = (char*)workspace;
+  HIP_TRY(timed(DIT_K_OTHER, 0, 0, hs, [&]() {
+    return launch_cond_embed(s->batch, s->hidden, t, y, w_t1, b_t1, w_t2, b_t2, class_table, (float*)(ws + L.feat),
+                             (float*)(ws + L.h1), cond, s->dtype, hs);
+  }));
+  return DIT_OK;
+}
+
+dit_status dit_pos_embed_2d(int32_t grid_h, int32_t grid_w, int32_t hidden, float* pos, void* stream) {
+  if (grid_h < 1 || grid_w < 1 || hidden < 4 || hidden % 4 != 0)
+    return fail(DIT_ERR_INVALID_ARG, "grid (%d x %d) must be >= 1 and hidden (%d) a positive multiple of 4", grid_h,
+                grid_w, hidden);
+  if ((long)grid_h * grid_w * hidden >= (1L << 31)) return fail(DIT_ERR_UNSUPPORTED, "position table too large");
+  if (!pos || !aligned(pos, 4)) return fail(DIT_ERR_INVALID_ARG, "pos NULL or misaligned");
+  HIP_TRY(launch_pos_embed_2d(grid_h, grid_w, hidden, pos, (hipStream_t)stream));
+  return DIT_OK;
+}
+
+dit_status dit_timing_enable(int kclass, int max_launches) {
+  if (kclass < 0 || kclass >= DIT_K_COUNT || max_launches < 1 || max_launches > (1 << 20))
+    return fail(DIT_ERR_INVALID_ARG, "bad timing class %d or launch count %d", kclass, max_launches);
+  dit_timing_disable();
+  std::lock_guard<std::mutex> lk(g_timing.mu);
+  g_timing.ev.assign(2 * (size_t)max_launches, nullptr);
+  for (auto& e : g_timing.ev) {
+    hipError_t r = hipEventCreate(&e);
+    if (r != hipSuccess) {
+      for (auto& f : g_timing.ev)
+        if (f) hipEventDestroy(f);
+      g_timing.ev.clear();
+      return fail(DIT_ERR_HIP, "hipEventCreate: %s", hipGetErrorString(r));
+    }
+  }
+  g_timing.kclass = kclass;
+  g_timing.max = max_launches;
+  g_timing.used = 0;
+  g_timing.flops = g_timing.bytes = 0;
+  return DIT_OK;
+}
+
+dit_status dit_timing_read(double* total_ms, int* launches, double* flops, double* bytes) {
+  std::lock_guard<std::mutex> lk(g_timing.mu);
+  double ms = 0;
+  for (int i = 0; i < g_timing.used; ++i) {
+    hipError_t r = hipEventSynchronize(g_timing.ev[2 * i + 1]);
+    if (r != hipSuccess) return fail(DIT_ERR_HIP, "hipEventSynchronize: %s", hipGetErrorString(r));
+    float t = 0;
+    r = hipEventElapsedTime(&t, g_timing.ev[2 * i], g_timing.ev[2 * i + 1]);
+    if (r != hipSuccess) return fail(DIT_ERR_HIP, "hipEventElapsedTime: %s", hipGetErrorString(r));
+    ms += t;
+  }
+  if (total_ms) *total_ms = ms;
+  if (launches) *launches = g_timing.used;
+  if (flops) *flops = g_timing.flops;
+  if (bytes) *bytes = g_timing.bytes;
+  return DIT_OK;
+}
+
+dit_status dit_timing_disable(void) {
+  std::lock_guard<std::mutex> lk(g_timing.mu);
+  for (auto& e : g_timing.ev)
+    if (e) hipEventDestroy(e);
+  g_timing.ev.clear();
+  g_timing.kclass = -1;
+  g_timing.max = g_timing.used = 0;
+  return DIT_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,315 @@
+// Memory-bound kernels of the DiT step on gfx950:
+//   * LayerNorm + adaLN modulate: h = LN(x) * (1 + scale) + shift, fp32 in,
+//     GEMM operand (bf16 or fp32) out; one wavefront per token row, 16-byte
+//     loads, exact two-pass mean/variance from registers.
+//   * adaLN modulation GEMV: m = SiLU(c) W_ada^T + b_ada for many (block,
+//     stream) weight matrices in one launch; HBM-bound on the weights.
+//   * timestep + class conditioning, patch embedding, 2-D sin-cos table.
+#include <math.h>
+
+#include "common.h"
+#include "kernels.h"
+
+namespace ditmi {
+
+// ---------------------------------------------------------------- LayerNorm + modulate
+template <typename OutT, int NV>
+__global__ __launch_bounds__(256) void ln_mod_kernel(LnArgs a) {
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (row >= a.total_rows) return;  // whole wavefront leaves together
+  const int si = (a.nseg > 1 && row >= a.s[1].row_begin) ? 1 : 0;
+  const LnSeg& S = a.s[si];
+  const int r = row - S.row_begin;
+  const int b = r / S.rows_per_batch;
+  const int D = a.D, nq = D >> 2;
+  const float4* __restrict__ xr = (const float4*)(S.x + (long)r * D);
+
+  float4 v[NV];
+  float sum = 0.f;
+#pragma unroll
+  for (int i = 0; i < NV; ++i) {
+    const int c = lane + 64 * i;
+    v[i] = c < nq ? xr[c] : make_float4(0.f, 0.f, 0.f, 0.f);
+    sum += (v[i].x + v[i].y) + (v[i].z + v[i].w);
+  }
+  const float mean = warp_sum(sum) / (float)D;
+  float sq = 0.f;
+#pragma unroll
+  for (int i = 0; i < NV; ++i) {
+    const int c = lane + 64 * i;
+    if (c < nq) {
+      const float dx = v[i].x - mean, dy = v[i].y - mean, dz = v[i].z - mean, dw = v[i].w - mean;
+      sq += (dx * dx + dy * dy) + (dz * dz + dw * dw);
+    }
+  }
+  const float var = warp_sum(sq) / (float)D;
+  const float rstd = 1.0f / sqrtf(var + a.eps);
+  const float4* __restrict__ sh = (const float4*)(S.shift + (long)b * S.mod_stride);
+  const float4* __restrict__ sc = (const float4*)(S.scale + (long)b * S.mod_stride);
+#pragma unroll
+  for (int i = 0; i < NV; ++i) {
+    const int c = lane + 64 * i;
+    if (c >= nq) continue;
+    const float4 s4 = sh[c], c4 = sc[c];
+    const float y0 = (v[i].x - mean) * rstd * (1.f + c4.x) + s4.x;
+    const float y1 = (v[i].y - mean) * rstd * (1.f + c4.y) + s4.y;
+    const float y2 = (v[i].z - mean) * rstd * (1.f + c4.z) + s4.z;
+    const float y3 = (v[i].w - mean) * rstd * (1.f + c4.w) + s4.w;
+    if constexpr (sizeof(OutT) == 2) {
+      uint2 w = make_uint2(pack_bf16x2(y0, y1), pack_bf16x2(y2, y3));
+      ((uint2*)S.out)[(long)r * nq + c] = w;
+    } else {
+      ((float4*)S.out)[(long)r * nq + c] = make_float4(y0, y1, y2, y3);
+    }
+  }
+}
+
+template <typename OutT>
+static hipError_t ln_dispatch(const LnArgs& a, hipStream_t st) {
+  dim3 grid((a.total_rows + 3) / 4), block(256);
+  const int nv = (a.D / 4 + 63) / 64;
+  if (nv <= 2) hipLaunchKernelGGL((ln_mod_kernel<OutT, 2>), grid, block, 0, st, a);
+  else if (nv <= 5) hipLaunchKernelGGL((ln_mod_kernel<OutT, 5>), grid, block, 0, st, a);
+  else if (nv <= 8) hipLaunchKernelGGL((ln_mod_kernel<OutT, 8>), grid, block, 0, st, a);
+  else if (nv <= 12) hipLaunchKernelGGL((ln_mod_kernel<OutT, 12>), grid, block, 0, st, a);
+  else hipLaunchKernelGGL((ln_mod_kernel<OutT, 16>), grid, block, 0, st, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_ln_mod(const LnArgs& a, int dtype, hipStream_t st) {
+  return dtype == 1 ? ln_dispatch<bf16_t>(a, st) : ln_dispatch<float>(a, st);
+}
+
+// ---------------------------------------------------------------- adaLN GEMV
+// Workgroup = 4 waves x 8 lane-groups x 4 rows = 128 output rows of one
+// entry.  A lane-group of 8 lanes reads 128 contiguous bytes of each of its
+// 4 weight rows per step; SiLU(c) for up to 8 samples sits in LDS and is
+// reused across the 4 rows.
+template <typename WT> struct W8;
+template <> struct W8<bf16_t> {
+  static __device__ __forceinline__ void load(const bf16_t* p, float* w) {
+    uint4 u = *(const uint4*)p;
+    uint32_t x[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      w[2 * i] = __uint_as_float(x[i] << 16);
+      w[2 * i + 1] = __uint_as_float(x[i] & 0xFFFF0000u);
+    }
+  }
+};
+template <> struct W8<float> {
+  static __device__ __forceinline__ void load(const float* p, float* w) {
+    float4 u0 = *(const float4*)p, u1 = *(const float4*)(p + 4);
+    w[0] = u0.x; w[1] = u0.y; w[2] = u0.z; w[3] = u0.w;
+    w[4] = u1.x; w[5] = u1.y; w[6] = u1.z; w[7] = u1.w;
+  }
+};
+
+template <typename WT>
+__global__ __launch_bounds__(256) void adaln_kernel(AdaArgs a) {
+  extern __shared__ float sc[];  // [min(B, 8)][D]
+  const int wg = blockIdx.x;
+  int ei = 0;
+  while (ei + 1 < a.ne && wg >= a.e[ei + 1].wg_begin) ++ei;
+  const AdaEntry& E = a.e[ei];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int grp = lane >> 3, li = lane & 7;
+  const int nbase = (wg - E.wg_begin) * 128 + wave * 32 + grp * 4;
+  const WT* __restrict__ W = (const WT*)E.W;
+  const WT* __restrict__ bias = (const WT*)E.bias;
+  const int D = a.D, nch = D >> 3, N = E.N;
+
+  for (int b0 = 0; b0 < a.B; b0 += 8) {
+    const int nb = min(8, a.B - b0);
+    __syncthreads();
+    for (int i = tid; i < nb * D; i += 256) {
+      const float z = a.cond[(long)b0 * D + i];
+      sc[i] = z / (1.0f + expf(-z));
+    }
+    __syncthreads();
+    float acc[4][8];
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+#pragma unroll
+      for (int bb = 0; bb < 8; ++bb) acc[r][bb] = 0.f;
+    for (int ci = li; ci < nch; ci += 8) {
+      float w[4][8];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int n = nbase + r;
+        if (n < N) W8<WT>::load(W + (long)n * D + ci * 8, w[r]);
+        else
+#pragma unroll
+          for (int e = 0; e < 8; ++e) w[r][e] = 0.f;
+      }
+#pragma unroll
+      for (int bb = 0; bb < 8; ++bb) {
+        if (bb < nb) {
+          const float4 s0 = *(const float4*)&sc[bb * D + ci * 8];
+          const float4 s1 = *(const float4*)&sc[bb * D + ci * 8 + 4];
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            float t = acc[r][bb];
+            t = fmaf(w[r][0], s0.x, t); t = fmaf(w[r][1], s0.y, t);
+            t = fmaf(w[r][2], s0.z, t); t = fmaf(w[r][3], s0.w, t);
+            t = fmaf(w[r][4], s1.x, t); t = fmaf(w[r][5], s1.y, t);
+            t = fmaf(w[r][6], s1.z, t); t = fmaf(w[r][7], s1.w, t);
+            acc[r][bb] = t;
+          }
+        }
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+#pragma unroll
+      for (int bb = 0; bb < 8; ++bb) {
+        float t = acc[r][bb];
+        t += __shfl_xor(t, 1, 64);
+        t += __shfl_xor(t, 2, 64);
+        t += __shfl_xor(t, 4, 64);
+        acc[r][bb] = t;
+      }
+    // lane li of the group writes sample b0 + li
+    if (li < nb) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int n = nbase + r;
+        if (n >= N) continue;
+        float val = 0.f;
+#pragma unroll
+        for (int bb = 0; bb < 8; ++bb) val = (bb == li) ? acc[r][bb] : val;
+        E.out[(long)(b0 + li) * N + n] = val + ld_as_float<WT>(bias, n);
+      }
+    }
+  }
+}
+
+hipError_t launch_adaln(const AdaArgs& a, int dtype, hipStream_t st) {
+  const size_t lds = (size_t)(a.B < 8 ? a.B : 8) * a.D * sizeof(float);
+  dim3 grid(a.total_wg), block(256);
+  if (dtype == 1) {
+    hipError_t e = hipFuncSetAttribute((const void*)adaln_kernel<bf16_t>,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((adaln_kernel<bf16_t>), grid, block, lds, st, a);
+  } else {
+    hipError_t e = hipFuncSetAttribute((const void*)adaln_kernel<float>,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((adaln_kernel<float>), grid, block, lds, st, a);
+  }
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- conditioning
+// feat[b][i] = cos(t_b f_i) (i < 128), sin(t_b f_{i-128}) (i >= 128),
+// f_i = exp(-ln(10000) i / 128); evaluated in double for the large arguments.
+__global__ void timestep_feat_kernel(int B, const float* t, float* feat) {
+  const int idx = blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= B * 256) return;
+  const int b = idx >> 8, i = idx & 255;
+  const int fi = i & 127;
+  const double f = exp(-9.210340371976184 * (double)fi / 128.0);  // ln(10000)
+  const double arg = (double)t[b] * f;
+  feat[idx] = (float)(i < 128 ? cos(arg) : sin(arg));
+}
+
+// out[b][n] = post(sum_k W[n][k] in[b][k] + bias[n]); one wavefront per row n.
+// MODE 0: post = SiLU.  MODE 1: post = identity, plus class_table[y[b]][n].
+template <typename WT, int MODE>
+__global__ __launch_bounds__(256) void rowdot_kernel(int B, int N, int K, const float* in, const WT* W,
+                                                     const WT* bias, const WT* table, const int32_t* y,
+                                                     float* out) {
+  const int n = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (n >= N) return;
+  const WT* wr = W + (long)n * K;
+  for (int b = 0; b < B; ++b) {
+    float acc = 0.f;
+    for (int k = lane; k < K; k += 64) acc = fmaf(ld_as_float<WT>(wr, k), in[(long)b * K + k], acc);
+    acc = warp_sum(acc) + ld_as_float<WT>(bias, n);
+    if (lane == 0) {
+      if (MODE == 0) out[(long)b * N + n] = acc / (1.0f + expf(-acc));
+      else out[(long)b * N + n] = acc + ld_as_float<WT>(table, (long)y[b] * N + n);
+    }
+  }
+}
+
+hipError_t launch_cond_embed(int B, int D, const float* t, const int32_t* y, const void* w1, const void* b1,
+                             const void* w2, const void* b2, const void* table, float* feat, float* h1,
+                             float* cond, int dtype, hipStream_t st) {
+  hipLaunchKernelGGL(timestep_feat_kernel, dim3((B * 256 + 255) / 256), dim3(256), 0, st, B, t, feat);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  dim3 grid((D + 3) / 4), block(256);
+  if (dtype == 1) {
+    hipLaunchKernelGGL((rowdot_kernel<bf16_t, 0>), grid, block, 0, st, B, D, 256, feat, (const bf16_t*)w1,
+                       (const bf16_t*)b1, (const bf16_t*)nullptr, (const int32_t*)nullptr, h1);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL((rowdot_kernel<bf16_t, 1>), grid, block, 0, st, B, D, D, h1, (const bf16_t*)w2,
+                       (const bf16_t*)b2, (const bf16_t*)table, y, cond);
+  } else {
+    hipLaunchKernelGGL((rowdot_kernel<float, 0>), grid, block, 0, st, B, D, 256, feat, (const float*)w1,
+                       (const float*)b1, (const float*)nullptr, (const int32_t*)nullptr, h1);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL((rowdot_kernel<float, 1>), grid, block, 0, st, B, D, D, h1, (const float*)w2,
+                       (const float*)b2, (const float*)table, y, cond);
+  }
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- patch embedding
+// x[row][n] = sum_p z[row][p] W[n][p] + bias[n] (+ pos[row % T][n]); one
+// workgroup per token row, the patch vector staged in LDS.
+template <typename WT>
+__global__ __launch_bounds__(256) void patch_embed_kernel(int T, int P, int D, const float* z, const WT* w,
+                                                          const WT* bias, const float* pos, float* x) {
+  __shared__ float zs[256];
+  const int row = blockIdx.x, tid = threadIdx.x;
+  if (tid < P) zs[tid] = z[(long)row * P + tid];
+  __syncthreads();
+  const int t = row % T;
+  for (int n = tid; n < D; n += 256) {
+    float acc = ld_as_float<WT>(bias, n);
+    const WT* wr = w + (long)n * P;
+    for (int p = 0; p < P; ++p) acc = fmaf(ld_as_float<WT>(wr, p), zs[p], acc);
+    if (pos) acc += pos[(long)t * D + n];
+    x[(long)row * D + n] = acc;
+  }
+}
+
+hipError_t launch_patch_embed(int rows, int T, int P, int D, const float* z, const void* w, const void* b,
+                              const float* pos, float* x, int dtype, hipStream_t st) {
+  if (dtype == 1)
+    hipLaunchKernelGGL((patch_embed_kernel<bf16_t>), dim3(rows), dim3(256), 0, st, T, P, D, z,
+                       (const bf16_t*)w, (const bf16_t*)b, pos, x);
+  else
+    hipLaunchKernelGGL((patch_embed_kernel<float>), dim3(rows), dim3(256), 0, st, T, P, D, z,
+                       (const float*)w, (const float*)b, pos, x);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- 2-D sin-cos table
+__global__ void pos_embed_2d_kernel(int gh, int gw, int D, float* pos) {
+  const long idx = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  const long total = (long)gh * gw * D;
+  if (idx >= total) return;
+  const int n = (int)(idx / D), dd = (int)(idx - (long)n * D);
+  const int r = n / gw, c = n - r * gw;
+  const int half = D / 2, q = D / 4;
+  const int p = dd < half ? c : r;
+  const int e = dd < half ? dd : dd - half;
+  const int i = e < q ? e : e - q;
+  const double omega = exp(-9.210340371976184 * (double)i / (double)q);  // 10000^(-i/q)
+  const double arg = (double)p * omega;
+  pos[idx] = (float)(e < q ? sin(arg) : cos(arg));
+}
+
+hipError_t launch_pos_embed_2d(int gh, int gw, int D, float* pos, hipStream_t st) {
+  const long total = (long)gh * gw * D;
+  hipLaunchKernelGGL(pos_embed_2d_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, st, gh, gw, D, pos);
+  return hipGetLastError();
+}
+
+}  // namespace ditmi

@@ -1,0 +1,103 @@
+// Internal launch interface between the host sequencer (ditmi.cpp) and the
+// gfx950 kernels.  Argument structs are passed to kernels by value.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace ditmi {
+
+// ------------------------------------------------------------------ GEMM
+// y[M, N] = A[M, K] * W[N, K]^T (+ bias), K-contiguous operands, then one of:
+enum Epi {
+  EPI_QKV = 0,    // +bias; scatter into head-major q, k and (bf16: transposed) v
+  EPI_GELU = 1,   // +bias; tanh-GELU; store in the operand type
+  EPI_RESID = 2,  // +bias; resid[m, n] += gate[b, n] * y   (fp32 residual stream)
+  EPI_STORE = 3   // +bias; store fp32
+};
+
+struct GemmProb {
+  const void* A;      // [M, K]
+  const void* W;      // [N, K]
+  const void* bias;   // [N]
+  int M, N, K;
+  int tiles_m, tiles_n, tile_begin;
+  int rows_per_batch;  // sample index b = m / rows_per_batch
+  // EPI_RESID
+  float* resid;
+  const float* gate;   // gate[b * gate_stride + n]
+  int gate_stride;
+  // EPI_GELU / EPI_STORE
+  void* out;           // [M, N] row-major
+  // EPI_QKV: row m -> (b, j = m % rows_per_batch + seq_off) of the joint sequence
+  void* q;             // [B, H, Tj, dh]
+  void* k;             // [B, H, Tj, dh]
+  void* v;             // bf16: v^T [B, H, dh, Tj_pad]; fp32: [B, H, Tj, dh]
+  int seq_off, Tj, Tj_pad, heads, head_dim, hidden;
+};
+
+struct GemmArgs {
+  GemmProb p[2];
+  int nprob;
+  int total_tiles;
+};
+
+// ------------------------------------------------------------------ attention
+struct AttnArgs {
+  const void* q;   // [B, H, Tj, dh]
+  const void* k;   // [B, H, Tj, dh]
+  const void* v;   // bf16: v^T [B, H, dh, Tj_pad]; fp32: [B, H, Tj, dh]
+  void* o;         // stream-major rows: image b*T + t, then text B*T + b*Tt + t; [*, H*dh]
+  int B, H, Tj, Tj_pad, T_img, T_txt, D;
+  float scale_log2;  // log2(e) / sqrt(dh)
+  float scale;       // 1 / sqrt(dh)
+};
+
+// ------------------------------------------------------------------ LayerNorm + modulate
+struct LnSeg {
+  const float* x;       // [rows, D] fp32
+  void* out;            // [rows, D] operand type
+  const float* shift;   // shift[b * mod_stride + n]
+  const float* scale;   // scale[b * mod_stride + n]
+  int rows, rows_per_batch, mod_stride, row_begin;
+};
+struct LnArgs {
+  LnSeg s[2];
+  int nseg, D, total_rows;
+  float eps;
+};
+
+// ------------------------------------------------------------------ adaLN GEMV
+constexpr int ADA_MAX_ENTRIES = 64;
+struct AdaEntry {
+  const void* W;     // [N, D]
+  const void* bias;  // [N]
+  float* out;        // [B, N]
+  int N, wg_begin;
+};
+struct AdaArgs {
+  AdaEntry e[ADA_MAX_ENTRIES];
+  int ne, total_wg;
+  const float* cond;  // [B, D]
+  int B, D;
+};
+
+// ------------------------------------------------------------------ launchers
+// Each returns hipSuccess or the launch error.  dtype: 0 = fp32, 1 = bf16.
+hipError_t launch_gemm_bf16(const GemmArgs& a, int epi, int tile_cfg, hipStream_t st);
+hipError_t launch_gemm_f32(const GemmArgs& a, int epi, hipStream_t st);
+hipError_t launch_attn_bf16(const AttnArgs& a, int head_dim, hipStream_t st);
+hipError_t launch_attn_f32(const AttnArgs& a, int head_dim, hipStream_t st);
+hipError_t launch_ln_mod(const LnArgs& a, int dtype, hipStream_t st);
+hipError_t launch_adaln(const AdaArgs& a, int dtype, hipStream_t st);
+hipError_t launch_cond_embed(int B, int D, const float* t, const int32_t* y, const void* w1, const void* b1,
+                             const void* w2, const void* b2, const void* table, float* feat, float* h1,
+                             float* cond, int dtype, hipStream_t st);
+hipError_t launch_patch_embed(int rows, int T, int P, int D, const float* z, const void* w, const void* b,
+                              const float* pos, float* x, int dtype, hipStream_t st);
+hipError_t launch_pos_embed_2d(int gh, int gw, int D, float* pos, hipStream_t st);
+
+// Tile configurations of the bf16 GEMM (BM x BN).
+enum { TILE_128x128 = 0, TILE_64x128 = 1, TILE_128x64 = 2, TILE_64x64 = 3, TILE_COUNT = 4 };
+void gemm_tile_dims(int tile_cfg, int* bm, int* bn);
+
+}  // namespace ditmi

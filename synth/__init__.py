@@ -100,7 +100,7 @@ STREAM_IMG, STREAM_TXT = 0, 1
 
 
 def _rng(cfg: DiTConfig, block: int, tensor_id: int, salt: int = 0) -> np.random.Generator:
-    return np.random.default_rng(np.random.SeedSequence([SEED_ROOT, cfg.index, block + 1, tensor_id, salt]))
+    return np.random.default_rng(np.random.SeedSequence([SEED_ROOT, cfg.index, block + 2, tensor_id, salt]))
 
 
 def bf16_round(a: np.ndarray) -> np.ndarray:

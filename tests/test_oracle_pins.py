@@ -411,3 +411,16 @@ def test_generator_is_deterministic_and_bf16_representable():
     c = synth.stream_weights(cfg, 4)
     assert not np.array_equal(a["w_qkv"], c["w_qkv"])
     assert abs(float(a["w_fc1"].std()) - 0.02) < 0.002
+
+
+def test_generator_inputs_all_configs():
+    for key, cfg in synth.CONFIGS.items():
+        small = cfg.with_(tokens=min(cfg.tokens, 32))
+        inp = synth.inputs(small)
+        assert inp["x"].shape == (small.batch, small.tokens, small.hidden)
+        assert inp["cond"].shape == (small.batch, small.hidden)
+        assert ("x_txt" in inp) == small.joint
+        if small.cond == "class":
+            assert np.all((inp["t"] >= 0) & (inp["t"] < 1000)) and np.all((inp["y"] >= 0) & (inp["y"] < 1000))
+        np.testing.assert_array_equal(synth.inputs(small)["x"], inp["x"])
+        assert not np.array_equal(synth.inputs(small, salt=1)["x"], inp["x"])

@@ -1,0 +1,203 @@
+"""GPU parity of the HIP path (through the C ABI) against the fp64 oracle on
+the same seeded inputs.
+
+Metric: err = max|gpu - oracle| / max|oracle| over the compared tensor,
+applied to the block output y AND to the branch increment y - x (the exact
+pass-through of x would otherwise hide branch errors).  Bars: 2e-2 for the
+bf16 path, 1e-4 for the fp32 path.
+"""
+import numpy as np
+import pytest
+import torch
+
+import synth
+from oracle import dit_oracle as O
+
+pytestmark = pytest.mark.gpu
+
+TOL = {"bf16": 2e-2, "f32": 1e-4}
+
+
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from tests import gpu_util
+    return gpu_util
+
+
+def f64(w):
+    return {k: v.astype(np.float64) for k, v in w.items()}
+
+
+def check(name, got, ref, base, tol):
+    e_y = O.rel_err(got, ref)
+    e_d = O.rel_err(got - base, ref - base) if base is not None else e_y
+    print(f"[parity] {name}: err_y={e_y:.3e} err_delta={e_d:.3e} tol={tol:g}", flush=True)
+    assert np.all(np.isfinite(got)), name
+    assert e_y <= tol and e_d <= tol, (name, e_y, e_d)
+
+
+def block_case(cfg, salt=0, rows=None):
+    g = _gpu()
+    w = synth.block_weights(cfg, 0)
+    inp = synth.inputs(cfg, salt)
+    x, c = inp["x"], inp["cond"]
+    xt = inp.get("x_txt")
+    y, yt = g.run_block(cfg, w, x, c, xt)
+    tol = TOL[cfg.dtype]
+    if cfg.joint:
+        ry, ryt = O.joint_block(x, xt, c, f64(w["img"]), f64(w["txt"]), cfg.heads, cfg.ln_eps, rows_img=rows)
+        sel = slice(None) if rows is None else rows
+        check(f"{cfg.key}/img", y[:, sel], ry, x[:, sel], tol)
+        check(f"{cfg.key}/txt", yt, ryt, xt, tol)
+    else:
+        ry = O.dit_block(x, c, f64(w["img"]), cfg.heads, cfg.ln_eps, rows=rows)
+        sel = slice(None) if rows is None else rows
+        check(cfg.key, y[:, sel], ry, x[:, sel], tol)
+
+
+# ------------------------------------------------------------------ small (oracle-fast) shapes
+SMALL = [
+    ("c0_full_fp32", synth.CONFIGS["c0"]),
+    ("fp32_dh72_ragged", synth.CONFIGS["c0"].with_(tokens=77, hidden=576, heads=8, head_dim=72, mlp_hidden=256, batch=2)),
+    ("fp32_dh128_joint", synth.CONFIGS["c0"].with_(tokens=40, text_tokens=9, hidden=256, heads=2, head_dim=128,
+                                                   mlp_hidden=512, batch=2)),
+    ("bf16_dh72_t200_b2", synth.CONFIGS["c1"].with_(batch=2, tokens=200, n_blocks=1)),
+    ("bf16_dh64_t130", synth.CONFIGS["c1"].with_(batch=1, tokens=130, hidden=256, heads=4, head_dim=64,
+                                                 mlp_hidden=1024, n_blocks=1)),
+    ("bf16_dh128_t150_b2", synth.CONFIGS["c1"].with_(batch=2, tokens=150, hidden=256, heads=2, head_dim=128,
+                                                     mlp_hidden=1024, n_blocks=1)),
+    ("bf16_t1", synth.CONFIGS["c1"].with_(batch=3, tokens=1, hidden=256, heads=2, head_dim=128, mlp_hidden=512, n_blocks=1)),
+    ("bf16_t17", synth.CONFIGS["c1"].with_(batch=2, tokens=17, hidden=576, heads=8, head_dim=72, mlp_hidden=256, n_blocks=1)),
+    ("bf16_t65_m_tail", synth.CONFIGS["c1"].with_(batch=1, tokens=65, hidden=192, heads=3, head_dim=64, mlp_hidden=320, n_blocks=1)),
+    ("bf16_t257", synth.CONFIGS["c1"].with_(batch=1, tokens=257, hidden=256, heads=2, head_dim=128, mlp_hidden=512, n_blocks=1)),
+    ("bf16_joint_t130_tt21_b2", synth.CONFIGS["c3"].with_(batch=2, tokens=130, text_tokens=21, hidden=256, heads=2,
+                                                          head_dim=128, mlp_hidden=1024, n_blocks=1)),
+    ("bf16_joint_dh72_tt5", synth.CONFIGS["c3"].with_(batch=1, tokens=64, text_tokens=5, hidden=576, heads=8,
+                                                      head_dim=72, mlp_hidden=256, n_blocks=1)),
+]
+
+
+@pytest.mark.parametrize("name,cfg", SMALL, ids=[s[0] for s in SMALL])
+def test_block_small(name, cfg):
+    print(f"[case] block {name} B={cfg.batch} T={cfg.tokens} Tt={cfg.text_tokens} D={cfg.hidden} "
+          f"dh={cfg.head_dim} {cfg.dtype}", flush=True)
+    block_case(cfg)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_zero_gates_identity_bitwise(dtype):
+    g = _gpu()
+    cfg = synth.CONFIGS["c1"].with_(batch=2, tokens=70, text_tokens=6, hidden=256, heads=2, head_dim=128,
+                                    mlp_hidden=512, n_blocks=1, dtype=dtype)
+    w = synth.block_weights(cfg, 0)
+    w = {"img": g.zero_gates(w["img"], cfg.hidden), "txt": g.zero_gates(w["txt"], cfg.hidden)}
+    inp = synth.inputs(cfg)
+    y, yt = g.run_block(cfg, w, inp["x"], inp["cond"], inp["x_txt"])
+    assert np.array_equal(y, inp["x"].astype(np.float64))
+    assert np.array_equal(yt, inp["x_txt"].astype(np.float64))
+
+
+def test_determinism_bitwise():
+    g = _gpu()
+    cfg = synth.CONFIGS["c1"].with_(batch=2, tokens=300, n_blocks=1)
+    w = synth.block_weights(cfg, 0)
+    inp = synth.inputs(cfg)
+    (y1, _), (y2, _) = g.run_block(cfg, w, inp["x"], inp["cond"], repeat=2)
+    assert np.array_equal(y1, y2)
+
+
+def test_cond_embed_and_pos_table():
+    g = _gpu()
+    import paper_2605_25550_amd as dm
+    cfg = synth.CONFIGS["c1"]
+    sw = synth.step_weights(cfg)
+    inp = synth.inputs(cfg)
+    shape = dm.shape_of(cfg)
+    dt = dm.weight_dtype(shape)
+    wd = {k: g.dev(sw[k], dt) for k in ("w_t1", "b_t1", "w_t2", "b_t2", "class_table")}
+    cond = torch.empty((cfg.batch, cfg.hidden), dtype=torch.float32, device="cuda")
+    ws = dm.alloc_workspace(shape, dm.DIT_WS_COND)
+    dm.cond_embed(shape, g.dev(inp["t"]), g.dev(inp["y"], torch.int32), wd, cond, ws)
+    ref = O.class_conditioning(inp["t"], inp["y"], *[sw[k].astype(np.float64) for k in
+                                                      ("w_t1", "b_t1", "w_t2", "b_t2", "class_table")])
+    check("cond_embed", g.host(cond), ref, None, 2e-3)
+    for gh, gw, D in ((16, 16, 1152), (32, 32, 1152), (3, 5, 8)):
+        pos = torch.empty((gh * gw, D), dtype=torch.float32, device="cuda")
+        dm.pos_embed_2d(gh, gw, D, pos)
+        torch.cuda.synchronize()
+        assert np.max(np.abs(g.host(pos) - O.pos_embed_2d(gh, gw, D))) < 1e-6
+
+
+# ------------------------------------------------------------------ step (small)
+STEP_SMALL = [
+    ("fp32_step_l2", synth.CONFIGS["c0"].with_(n_blocks=2, batch=2, tokens=64, grid=(8, 8))),
+    ("bf16_step_class_l3", synth.CONFIGS["c1"].with_(n_blocks=3, batch=2, tokens=64, hidden=256, heads=2,
+                                                     head_dim=128, mlp_hidden=512, grid=(8, 8))),
+    ("bf16_step_joint_l2", synth.CONFIGS["c3"].with_(n_blocks=2, batch=1, tokens=96, text_tokens=7, hidden=256,
+                                                     heads=2, head_dim=128, mlp_hidden=512)),
+]
+
+
+def step_ref(cfg, sw, blocks, inp, pos, c):
+    out, xt = O.dit_step(cfg, inp["patches"], c, {k: v.astype(np.float64) for k, v in sw.items()},
+                         [{k: f64(v) for k, v in b.items()} for b in blocks], x_txt=inp.get("x_txt"), pos=pos)
+    return out, xt
+
+
+@pytest.mark.parametrize("name,cfg", STEP_SMALL, ids=[s[0] for s in STEP_SMALL])
+def test_step_small(name, cfg):
+    g = _gpu()
+    print(f"[case] step {name}", flush=True)
+    sw = synth.step_weights(cfg)
+    blocks = [synth.block_weights(cfg, l) for l in range(cfg.n_blocks)]
+    inp = synth.inputs(cfg)
+    pos = O.pos_embed_2d(*cfg.grid, cfg.hidden) if cfg.grid else None
+    c = inp["cond"]
+    ds = g.DeviceStep(cfg, blocks, sw)
+    out, xt = ds.run(inp["patches"], c, inp.get("x_txt"))
+    rout, rxt = step_ref(cfg, sw, blocks, inp, pos, c)
+    check(f"step/{name}", out, rout, None, TOL[cfg.dtype])
+    if cfg.joint:
+        check(f"step/{name}/txt", xt, rxt, inp["x_txt"], TOL[cfg.dtype])
+
+
+# ------------------------------------------------------------------ full-size shapes
+def test_block_c1_full():
+    block_case(synth.CONFIGS["c1"].with_(n_blocks=1))
+
+
+def test_block_c2_full():
+    block_case(synth.CONFIGS["c2"].with_(n_blocks=1))
+
+
+def test_block_c3_full_sampled_rows():
+    rows = [0, 1, 777, 2048, 4000, 4095]
+    block_case(synth.CONFIGS["c3"].with_(n_blocks=1), rows=rows)
+
+
+def test_block_c4_full_sampled_rows():
+    rows = [0, 5, 8191, 12000, 17536, 17549]
+    block_case(synth.CONFIGS["c4"].with_(n_blocks=1), rows=rows)
+
+
+def test_step_c1_full_end_to_end():
+    """Conditioning + the full 28-block step at the benchmarked workload."""
+    g = _gpu()
+    import paper_2605_25550_amd as dm
+    cfg = synth.CONFIGS["c1"]
+    sw = synth.step_weights(cfg)
+    inp = synth.inputs(cfg)
+    blocks = [synth.block_weights(cfg, l) for l in range(cfg.n_blocks)]
+    pos = O.pos_embed_2d(*cfg.grid, cfg.hidden)
+    ds = g.DeviceStep(cfg, blocks, sw)
+    shape = ds.shape
+    cond = torch.empty((cfg.batch, cfg.hidden), dtype=torch.float32, device="cuda")
+    wsc = dm.alloc_workspace(shape, dm.DIT_WS_COND)
+    dm.cond_embed(shape, g.dev(inp["t"]), g.dev(inp["y"], torch.int32),
+                  {k: ds.step[k] for k in ("w_t1", "b_t1", "w_t2", "b_t2", "class_table")}, cond, wsc)
+    out, _ = ds.run(inp["patches"], g.host(cond).astype(np.float32))
+    c = O.class_conditioning(inp["t"], inp["y"], *[sw[k].astype(np.float64) for k in
+                                                    ("w_t1", "b_t1", "w_t2", "b_t2", "class_table")])
+    rout, _ = step_ref(cfg, sw, blocks, inp, pos, c)
+    check("step/c1_full", out, rout, None, TOL["bf16"])
