@@ -1,0 +1,332 @@
+"""Throughput of the DiT denoising step on one MI355X.
+
+Workload: DiT-XL/2 at a 32x32x4 latent (256 tokens), batch 8, 28 blocks,
+hidden 1152, 16 heads x 72, MLP 4608, bf16 weights and GEMM operands with
+fp32 accumulation, timestep + class conditioning.  One step = conditioning
+embedding + patch embedding + 28 DiT blocks + final layer, all in the HIP
+library (include/ditmi.h), inputs resident in HBM.  Weights are random-init
+(N(0, 0.02), drawn on the device), latents N(0, 1).
+
+Prints ONE JSON line with steps/s, the roofline of the dominant kernel
+(measured with HIP events around its launches on the launch stream during
+the timed region) and the fp64 CPU oracle timed on a bounded sample.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "DiT denoising steps/sec at 1 GPU; GEMM+attention TFLOP/s as % of bf16 MFMA peak"
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0
+CSRC = os.path.join(ROOT, "paper_2605_25550_amd", "csrc")
+PROFILES = os.path.join(ROOT, "profiles")
+
+# kernel class -> (regex of its kernel symbol in rocprofv3 output, source file).  The
+# GEMM classes differ in the last template argument (the fused epilogue).
+CLASSES = {
+    "gemm_qkv": (r"gemm_bf16_kernel<\d+, \d+, \d+, 0>", "gemm_bf16.hip"),
+    "attention": (r"attn_bf16_kernel<", "attention_bf16.hip"),
+    "gemm_out": (r"gemm_bf16_kernel<\d+, \d+, \d+, 2>", "gemm_bf16.hip"),
+    "gemm_fc1": (r"gemm_bf16_kernel<\d+, \d+, \d+, 1>", "gemm_bf16.hip"),
+    "gemm_fc2": (r"gemm_bf16_kernel<\d+, \d+, \d+, 4>", "gemm_bf16.hip"),
+    "ln_mod": (r"ln_mod_kernel<", "elementwise.hip"),
+    "adaln": (r"adaln_kernel<", "elementwise.hip"),
+}
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--config", default="c1", help="workload key (c1 is the reported one)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-blocks", type=int, default=28, help="oracle blocks in the CPU sample")
+    ap.add_argument("--copy-probe-mib", type=int, default=0,
+                    help="also run a plain device copy of this size (counter calibration runs)")
+    ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                    help="no GPU work: turn two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE) of this "
+                         "command with --copy-probe-mib into profiles/<kernel>_<workload>_traffic.json")
+    ap.add_argument("--kernel-class", default=None, help="kernel class for --summarize-pmc")
+    return ap.parse_args()
+
+
+def source_hash(fname: str) -> str:
+    h = hashlib.sha256()
+    for f in (fname, "common.h", "kernels.h"):
+        with open(os.path.join(CSRC, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def traffic_from_profile(kclass: str, workload: str):
+    """HBM bytes per launch from the committed counter summary, if it was taken
+    on the current kernel source; else None."""
+    path = os.path.join(PROFILES, f"{kclass}_{workload}_traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as fh:
+        rec = json.load(fh)
+    if rec.get("source_hash") != source_hash(CLASSES[kclass][1]):
+        return None
+    return rec.get("hbm_bytes_per_launch")
+
+
+def _pmc_rows(d):
+    import csv
+    import glob
+    rows = []
+    for f in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+        with open(f) as fh:
+            rows += list(csv.DictReader(fh))
+    return rows
+
+
+def summarize_pmc(fetch_dir, write_dir, kclass, workload, copy_mib):
+    """Per-launch HBM bytes of one kernel class from FETCH_SIZE / WRITE_SIZE
+    (KiB per dispatch), each scaled by what the counter reads for a plain copy of
+    copy_mib MiB (the largest copy dispatch of the run)."""
+    import re
+    pat = re.compile(CLASSES[kclass][0])
+    out = {"kernel_class": kclass, "workload": workload, "source_hash": source_hash(CLASSES[kclass][1])}
+    copy_bytes = copy_mib * (1 << 20)
+    for name, d, counter in (("fetch", fetch_dir, "FETCH_SIZE"), ("write", write_dir, "WRITE_SIZE")):
+        rows = [r for r in _pmc_rows(d) if r["Counter_Name"] == counter]
+        kern = [float(r["Counter_Value"]) * 1024 for r in rows if pat.search(r["Kernel_Name"])]
+        copies = [float(r["Counter_Value"]) * 1024 for r in rows
+                  if "elementwise" in r["Kernel_Name"] or "copy" in r["Kernel_Name"].lower()]
+        if not kern or not copies:
+            raise SystemExit(f"no {counter} rows for {kclass} or for the copy probe in {d}")
+        probe = max(copies)
+        factor = probe / copy_bytes   # counter bytes per true byte (read once, or written once)
+        out[f"{name}_counter_bytes_per_launch"] = sum(kern) / len(kern)
+        out[f"{name}_copy_counter_bytes"] = probe
+        out[f"{name}_factor"] = factor
+        out[f"{name}_bytes_per_launch"] = out[f"{name}_counter_bytes_per_launch"] / factor
+        out[f"{name}_launches"] = len(kern)
+    out["hbm_bytes_per_launch"] = out["fetch_bytes_per_launch"] + out["write_bytes_per_launch"]
+    path = os.path.join(PROFILES, f"{kclass}_{workload}_traffic.json")
+    with open(path, "w") as fh:
+        json.dump(out, fh, indent=1)
+    print(json.dumps(out))
+
+
+class Workload:
+    def __init__(self, cfg, torch, dm):
+        self.cfg = cfg
+        self.torch = torch
+        self.dm = dm
+        self.shape = dm.shape_of(cfg)
+        self.dt = dm.weight_dtype(self.shape)
+        D, F = cfg.hidden, cfg.mlp_hidden
+        g = torch.Generator(device="cuda")
+        g.manual_seed(2605)
+
+        def rnd(*s, std=0.02):
+            return (torch.randn(*s, device="cuda", generator=g) * std).to(self.dt)
+
+        def stream():
+            return {"w_ada": rnd(6 * D, D), "b_ada": rnd(6 * D), "w_qkv": rnd(3 * D, D), "b_qkv": rnd(3 * D),
+                    "w_o": rnd(D, D), "b_o": rnd(D), "w_fc1": rnd(F, D), "b_fc1": rnd(F), "w_fc2": rnd(D, F),
+                    "b_fc2": rnd(D)}
+
+        self.blocks, structs = [], []
+        for _ in range(cfg.n_blocks):
+            img = stream()
+            txt = stream() if cfg.joint else None
+            self.blocks.append((img, txt))
+            structs.append(dm.block_struct(img, txt, self.dt))
+        self.step_w = {"w_patch": rnd(D, cfg.patch_in), "b_patch": rnd(D), "w_ada_final": rnd(2 * D, D),
+                       "b_ada_final": rnd(2 * D), "w_final": rnd(cfg.patch_out, D), "b_final": rnd(cfg.patch_out)}
+        self.pos = None
+        if cfg.grid is not None:
+            self.pos = torch.empty((cfg.grid[0] * cfg.grid[1], D), dtype=torch.float32, device="cuda")
+            dm.pos_embed_2d(cfg.grid[0], cfg.grid[1], D, self.pos)
+        self.table = dm.StepWeightTable(self.step_w, structs, self.dt, self.pos)
+        self.ws = dm.alloc_workspace(self.shape, dm.DIT_WS_STEP)
+        B, T = cfg.batch, cfg.tokens
+        self.patches = torch.randn(B, T, cfg.patch_in, device="cuda", generator=g)
+        self.x_txt = torch.randn(B, cfg.text_tokens, D, device="cuda", generator=g) if cfg.joint else None
+        self.out = torch.empty(B, T, cfg.patch_out, device="cuda")
+        if cfg.cond == "class":
+            self.cond_w = {"w_t1": rnd(D, cfg.freq_dim), "b_t1": rnd(D), "w_t2": rnd(D, D), "b_t2": rnd(D),
+                           "class_table": rnd(cfg.n_classes + 1, D)}
+            self.t = torch.randint(0, 1000, (B,), device="cuda", generator=g).float()
+            self.y = torch.randint(0, cfg.n_classes, (B,), device="cuda", generator=g).int()
+            self.ws_cond = self.dm.alloc_workspace(self.shape, dm.DIT_WS_COND)
+            self.cond = torch.empty(B, D, device="cuda")
+        else:
+            self.cond = torch.randn(B, D, device="cuda", generator=g)
+
+    def step(self):
+        if self.cfg.cond == "class":
+            self.dm.cond_embed(self.shape, self.t, self.y, self.cond_w, self.cond, self.ws_cond)
+        self.dm.step_forward(self.shape, self.table, self.patches, self.cond, self.out, self.ws, x_txt=self.x_txt)
+
+
+def algorithmic_flops(cfg) -> float:
+    """GEMM (24 B T D^2 per stream-block) + attention (4 B Tj^2 D per block)."""
+    T, Tt, B, D = cfg.tokens, cfg.text_tokens, cfg.batch, cfg.hidden
+    return cfg.n_blocks * (24.0 * B * (T + Tt) * D * D + 4.0 * B * (T + Tt) ** 2 * D)
+
+
+def cpu_baseline(cfg, n_blocks_sample: int):
+    """fp64 oracle on the host: conditioning + patch embed + n_blocks_sample
+    blocks (one block's weights reused) + final layer at the full batch, scaled
+    to the full block count."""
+    import numpy as np
+    from threadpoolctl import threadpool_info
+
+    import synth
+    from oracle import dit_oracle as O
+
+    scfg = synth.CONFIGS[cfg.key]
+    bw = synth.block_weights(scfg, 0)
+    sw = {k: v.astype(np.float64) for k, v in synth.step_weights(scfg).items()}
+    blocks = [{k: {n: a.astype(np.float64) for n, a in v.items()} for k, v in bw.items()}] * n_blocks_sample
+    inp = synth.inputs(scfg)
+    pos = O.pos_embed_2d(*scfg.grid, scfg.hidden) if scfg.grid else None
+    t0 = time.perf_counter()
+    if scfg.cond == "class":
+        c = O.class_conditioning(inp["t"], inp["y"], sw["w_t1"], sw["b_t1"], sw["w_t2"], sw["b_t2"], sw["class_table"])
+    else:
+        c = inp["cond"]
+    t_cond = time.perf_counter() - t0
+    t1 = time.perf_counter()
+    passes = 0
+    while True:  # at least one pass, and at least ~10 s of oracle work
+        O.dit_step(scfg.with_(n_blocks=n_blocks_sample), inp["patches"], c, sw, blocks, x_txt=inp.get("x_txt"),
+                   pos=pos)
+        passes += 1
+        if time.perf_counter() - t1 >= 10.0:
+            break
+    t_step = (time.perf_counter() - t1) / passes
+    # per-block share of the sampled run, extrapolated to all blocks (prologue/epilogue counted once)
+    sec_per_step = t_cond + t_step * (scfg.n_blocks / n_blocks_sample)
+    threads = max((i.get("num_threads", 1) for i in threadpool_info()), default=1)
+    return {"value": 1.0 / sec_per_step, "unit": "steps/s", "cores": threads, "kind": "oracle",
+            "sample": f"fp64 numpy oracle, full batch {scfg.batch}: conditioning + patch embed + "
+                      f"{n_blocks_sample} of {scfg.n_blocks} blocks (one block's weights) + final layer, "
+                      f"{passes} pass(es) at {t_step:.2f} s each, scaled to {scfg.n_blocks} blocks "
+                      f"({sec_per_step:.2f} s/step)"}
+
+
+def main():
+    args = parse()
+    if args.summarize_pmc:
+        import synth
+        summarize_pmc(args.summarize_pmc[0], args.summarize_pmc[1], args.kernel_class,
+                      synth.CONFIGS[args.config].key, args.copy_probe_mib or 256)
+        return
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path (run with --gpus 1)",
+              file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    import paper_2605_25550_amd as dm
+    import synth
+
+    cfg = synth.CONFIGS[args.config]
+    if cfg.dtype != "bf16":
+        raise SystemExit("bench.py times the bf16 workloads (c1..c4)")
+    torch.cuda.set_device(0)
+    dm.lib()
+    wl = Workload(cfg, torch, dm)
+    st = torch.cuda.current_stream()
+
+    # warmup; afterwards measure each kernel class once to find the dominant one
+    for _ in range(args.warmup):
+        wl.step()
+    torch.cuda.synchronize()
+    share = {}
+    for k in CLASSES:
+        dm.timing_enable(k, 4096)
+        wl.step()
+        torch.cuda.synchronize()
+        ms, n, fl, by = dm.timing_read()
+        dm.timing_disable()
+        share[k] = ms
+    dominant = max(share, key=share.get)
+
+    # timed region: K steps between synchronisations, events on the launch stream;
+    # the dominant kernel's launches are bracketed by the library's timing hook.
+    dm.timing_enable(dominant, 8192)
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ev0.record(st)
+    for _ in range(args.steps):
+        wl.step()
+    ev1.record(st)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    gpu_ms = ev0.elapsed_time(ev1)
+    k_ms, k_n, k_flops, k_bytes = dm.timing_read()
+    dm.timing_disable()
+    ms_per_step = gpu_ms / args.steps
+
+    if args.copy_probe_mib:
+        n = args.copy_probe_mib * (1 << 20) // 4
+        a = torch.ones(n, device="cuda")
+        b = torch.empty_like(a)
+        b.copy_(a)
+        torch.cuda.synchronize()
+
+    per_launch_ms = k_ms / max(k_n, 1)
+    flops_per_launch = k_flops / max(k_n, 1)
+    bytes_per_launch = k_bytes / max(k_n, 1)
+    mfma_bound = dominant.startswith("gemm") or dominant == "attention"
+    if mfma_bound:
+        achieved = flops_per_launch / (per_launch_ms * 1e-3) / 1e12
+        roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(achieved / PEAK_BF16_TFLOPS, 4)}
+    else:
+        achieved = bytes_per_launch / (per_launch_ms * 1e-3) / 1e9
+        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": round(achieved / PEAK_HBM_GBS, 4)}
+    roof["traffic"] = traffic_from_profile(dominant, cfg.key)
+    roof["kernel"] = dominant
+    roof["launch_ms"] = round(per_launch_ms, 5)
+    roof["launches"] = k_n
+    roof["algorithmic_per_launch"] = flops_per_launch if mfma_bound else bytes_per_launch
+
+    flops = algorithmic_flops(cfg)
+    result = {
+        "metric": METRIC,
+        "value": round(1000.0 / ms_per_step, 3),
+        "unit": "steps/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": cfg.name, "blocks": cfg.n_blocks, "batch": cfg.batch, "tokens": cfg.tokens,
+                   "text_tokens": cfg.text_tokens, "hidden": cfg.hidden, "heads": cfg.heads,
+                   "head_dim": cfg.head_dim, "mlp_hidden": cfg.mlp_hidden, "conditioning": cfg.cond,
+                   "parallelism": "single GPU"},
+        "step_tflops": round(flops / (ms_per_step * 1e-3) / 1e12, 2),
+        "step_frac_of_bf16_peak": round(flops / (ms_per_step * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+        "wall_s_timed": round(wall, 3),
+        "kernel_ms_per_step": {k: round(v, 4) for k, v in share.items()},
+        "roofline": roof,
+    }
+    if not args.no_cpu_baseline and cfg.key in ("c1", "c2"):
+        result["cpu_baseline"] = cpu_baseline(cfg, min(args.cpu_blocks, cfg.n_blocks))
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -70,7 +70,8 @@ typedef enum { DIT_WS_BLOCK = 0, DIT_WS_STEP = 1, DIT_WS_COND = 2 } dit_ws_kind;
  *   mlp_hidden    F, multiple of 64
  *   n_blocks      L >= 1 (used by the step)
  *   patch_in      p*p*C channels of one latent patch (step), 1..256
- *   patch_out     channels predicted per token by the final layer (step), 1..256
+ *   patch_out     channels predicted per token by the final layer (step), a
+ *                 multiple of 4 in 4..256
  *   dtype         dit_dtype of weights and GEMM operands
  *   ln_eps        LayerNorm epsilon (> 0) */
 typedef struct {

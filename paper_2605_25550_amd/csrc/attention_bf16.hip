@@ -64,67 +64,58 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
       qf[s] = bf16x8{};
   }
 
-  uint4 rk[K_IT], rv[V_IT];
-  auto gload = [&](int kv0) {
-#pragma unroll
-    for (int i = 0; i < K_IT; ++i) {
-      const int c = tid + 256 * i;
-      const int key = c / KCH, dc = c - key * KCH;
-      rk[i] = make_uint4(0, 0, 0, 0);
-      if (c < BKV * KCH && kv0 + key < Tj && dc * 8 < DH)
-        rk[i] = *(const uint4*)(kp + (long)(kv0 + key) * DH + dc * 8);
-    }
-#pragma unroll
-    for (int i = 0; i < V_IT; ++i) {
-      const int c = tid + 256 * i;
-      const int d = c >> 3, key0 = kv0 + (c & 7) * 8;
-      rv[i] = make_uint4(0, 0, 0, 0);
-      if (c < DH * 8 && key0 < Tj) {
-        uint4 v = *(const uint4*)(vp + (long)d * Tjp + key0);
-        const int nv = Tj - key0;  // valid keys in this chunk
-        if (nv < 8) {
-          uint32_t w[4] = {v.x, v.y, v.z, v.w};
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            if (2 * e >= nv) w[e] = 0;
-            else if (2 * e + 1 >= nv) w[e] &= 0xFFFFu;
-          }
-          v = make_uint4(w[0], w[1], w[2], w[3]);
-        }
-        rv[i] = v;
-      }
-    }
-  };
-  auto lstore = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < K_IT; ++i) {
-      const int c = tid + 256 * i;
-      if (c < BKV * KCH) {
-        const int key = c / KCH, dc = c - key * KCH;
-        *(uint4*)&Ks[buf][key * KST + dc * 8] = rk[i];
-      }
-    }
-#pragma unroll
-    for (int i = 0; i < V_IT; ++i) {
-      const int c = tid + 256 * i;
-      if (c < DH * 8) *(uint4*)&Vs[buf][(c >> 3) * VST + (c & 7) * 8] = rv[i];
-    }
-  };
+  u32x4 rk[K_IT], rv[V_IT];
+  // Fetch one K / V^T tile (keys kv0 .. kv0+63) into registers; keys past the
+  // end and head_dim padding read as zero.
+#define ATT_GLOAD(kv0_)                                                                 \
+  do {                                                                                 \
+    const int kvb = (kv0_);                                                            \
+    _Pragma("unroll") for (int i = 0; i < K_IT; ++i) {                                 \
+      const int c = tid + 256 * i;                                                     \
+      const int key = c / KCH, dc = c - key * KCH;                                     \
+      rk[i] = u32x4{0u, 0u, 0u, 0u};                                                   \
+      if (c < BKV * KCH && kvb + key < Tj && dc * 8 < DH)                              \
+        rk[i] = *(const u32x4*)(kp + (long)(kvb + key) * DH + dc * 8);                 \
+    }                                                                                  \
+    _Pragma("unroll") for (int i = 0; i < V_IT; ++i) {                                 \
+      const int c = tid + 256 * i;                                                     \
+      const int d = c >> 3, key0 = kvb + (c & 7) * 8;                                  \
+      rv[i] = u32x4{0u, 0u, 0u, 0u};                                                   \
+      if (c < DH * 8 && key0 < Tj) {                                                   \
+        u32x4 v = *(const u32x4*)(vp + (long)d * Tjp + key0);                          \
+        const int nv = Tj - key0;                                                      \
+        if (nv < 8) {                                                                  \
+          _Pragma("unroll") for (int e = 0; e < 4; ++e) {                              \
+            if (2 * e >= nv) v[e] = 0u;                                                \
+            else if (2 * e + 1 >= nv) v[e] &= 0xFFFFu;                                 \
+          }                                                                            \
+        }                                                                              \
+        rv[i] = v;                                                                     \
+      }                                                                                \
+    }                                                                                  \
+  } while (0)
+#define ATT_LSTORE(buf_)                                                                \
+  do {                                                                                 \
+    _Pragma("unroll") for (int i = 0; i < K_IT; ++i) {                                 \
+      const int c = tid + 256 * i;                                                     \
+      if (c < BKV * KCH) {                                                             \
+        const int key = c / KCH, dc = c - key * KCH;                                   \
+        *(u32x4*)&Ks[buf_][key * KST + dc * 8] = rk[i];                                \
+      }                                                                                \
+    }                                                                                  \
+    _Pragma("unroll") for (int i = 0; i < V_IT; ++i) {                                 \
+      const int c = tid + 256 * i;                                                     \
+      if (c < DH * 8) *(u32x4*)&Vs[buf_][(c >> 3) * VST + (c & 7) * 8] = rv[i];        \
+    }                                                                                  \
+  } while (0)
 
   float m_run = -INFINITY, l_run = 0.f;
   f32x16 oacc[DT];
 #pragma unroll
   for (int t = 0; t < DT; ++t) oacc[t] = f32x16{};
 
-  const int nkv = (Tj + BKV - 1) / BKV;
-  gload(0);
-  lstore(0);
-  __syncthreads();
-  for (int it = 0; it < nkv; ++it) {
-    const int buf = it & 1, kv0 = it * BKV;
-    if (it + 1 < nkv) gload(kv0 + BKV);
-
-    // S^T[key][query] for 64 keys: two 32-key MFMA tiles.
+  // One key tile: S^T = K Q^T, online softmax, O^T += V^T P^T.
+  auto tile = [&](const int buf, const int kv0) {
     f32x16 sacc[2];
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt) {
@@ -171,24 +162,40 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
       const int kt = c >> 1, jb = (c & 1) * 2;
-      uint32_t pw[4];
+      u32x4 pw;
       pw[0] = pack_bf16x2(sacc[kt][jb * 4 + 0], sacc[kt][jb * 4 + 1]);
       pw[1] = pack_bf16x2(sacc[kt][jb * 4 + 2], sacc[kt][jb * 4 + 3]);
       pw[2] = pack_bf16x2(sacc[kt][jb * 4 + 4], sacc[kt][jb * 4 + 5]);
       pw[3] = pack_bf16x2(sacc[kt][jb * 4 + 6], sacc[kt][jb * 4 + 7]);
-      bf16x8 pb = __builtin_bit_cast(bf16x8, make_uint4(pw[0], pw[1], pw[2], pw[3]));
+      const bf16x8 pb = __builtin_bit_cast(bf16x8, pw);
 #pragma unroll
       for (int t = 0; t < DT; ++t) {
         const bf16_t* vrow = &Vs[buf][(t * 32 + r32) * VST + c * 16 + g * 4];
-        uint2 lo = *(const uint2*)vrow;
-        uint2 hi = *(const uint2*)(vrow + 8);
-        bf16x8 vf = __builtin_bit_cast(bf16x8, make_uint4(lo.x, lo.y, hi.x, hi.y));
-        oacc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pb, oacc[t], 0, 0, 0);
+        const u32x2 lo = *(const u32x2*)vrow;
+        const u32x2 hi = *(const u32x2*)(vrow + 8);
+        const u32x4 vw = {lo[0], lo[1], hi[0], hi[1]};
+        oacc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, vw), pb, oacc[t], 0, 0, 0);
       }
     }
-    if (it + 1 < nkv) lstore(buf ^ 1);
+  };
+
+  // The last tile is peeled so the in-loop prefetch is unconditional.
+  const int nkv = (Tj + BKV - 1) / BKV;
+  ATT_GLOAD(0);
+  ATT_LSTORE(0);
+  __syncthreads();
+  for (int it = 0; it + 1 < nkv; ++it) {
+    const int buf = it & 1;
+    ATT_GLOAD((it + 1) * BKV);
+    __builtin_amdgcn_sched_barrier(0);
+    tile(buf, it * BKV);
+    __builtin_amdgcn_sched_barrier(0);
+    ATT_LSTORE(buf ^ 1);
     __syncthreads();
   }
+  tile((nkv - 1) & 1, (nkv - 1) * BKV);
+#undef ATT_GLOAD
+#undef ATT_LSTORE
 
   const float l_tot = l_run + other_half(l_run);
   const float inv = 1.0f / l_tot;
@@ -202,10 +209,10 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
       for (int jj = 0; jj < 4; ++jj) {
         const int d = t * 32 + jj * 8 + g * 4;
         if (d < DH) {
-          uint2 w;
-          w.x = pack_bf16x2(oacc[t][jj * 4 + 0] * inv, oacc[t][jj * 4 + 1] * inv);
-          w.y = pack_bf16x2(oacc[t][jj * 4 + 2] * inv, oacc[t][jj * 4 + 3] * inv);
-          *(uint2*)(op + d) = w;
+          u32x2 w;
+          w[0] = pack_bf16x2(oacc[t][jj * 4 + 0] * inv, oacc[t][jj * 4 + 1] * inv);
+          w[1] = pack_bf16x2(oacc[t][jj * 4 + 2] * inv, oacc[t][jj * 4 + 3] * inv);
+          *(u32x2*)(op + d) = w;
         }
       }
   }

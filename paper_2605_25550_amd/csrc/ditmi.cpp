@@ -60,9 +60,9 @@ dit_status check_shape(const dit_shape* s, bool step) {
     return fail(DIT_ERR_UNSUPPORTED, "batch*tokens (%ld rows) too large", rows);
   if (step) {
     if (s->n_blocks < 1) return fail(DIT_ERR_INVALID_ARG, "n_blocks (%d) must be >= 1", s->n_blocks);
-    if (s->patch_in < 1 || s->patch_in > 256 || s->patch_out < 1 || s->patch_out > 256)
-      return fail(DIT_ERR_INVALID_ARG, "patch_in (%d) and patch_out (%d) must be in [1, 256]", s->patch_in,
-                  s->patch_out);
+    if (s->patch_in < 1 || s->patch_in > 256 || s->patch_out < 4 || s->patch_out > 256 || s->patch_out % 4 != 0)
+      return fail(DIT_ERR_INVALID_ARG, "patch_in (%d) must be in [1, 256] and patch_out (%d) a multiple of 4 in [4, 256]",
+                  s->patch_in, s->patch_out);
   }
   return DIT_OK;
 }
@@ -112,7 +112,7 @@ dit_status check_stream_weights(const dit_stream_weights& w, const char* which) 
   for (const void* p : mats)
     if (!p || !aligned(p, 16)) return fail(DIT_ERR_INVALID_ARG, "%s weight matrix NULL or not 16-byte aligned", which);
   for (const void* p : vecs)
-    if (!p || !aligned(p, 4)) return fail(DIT_ERR_INVALID_ARG, "%s bias NULL or misaligned", which);
+    if (!p || !aligned(p, 16)) return fail(DIT_ERR_INVALID_ARG, "%s bias NULL or not 16-byte aligned", which);
   return DIT_OK;
 }
 
@@ -155,25 +155,18 @@ struct Gemm {
   double flops = 0, bytes = 0;
 };
 
-// Pick the bf16 tile shape that minimises (waves of 256 tiles) x (tile work /
-// tile efficiency); larger tiles reuse more operand bytes per MFMA.
+// bf16 tile choice (measured on MI355X): 128x128 tiles are the most
+// efficient per CU; when they would leave most CUs idle on a short K loop,
+// smaller tiles spread the work over more CUs.
 int choose_tile(const GemmProb* p, int np) {
-  static const double eff[TILE_COUNT] = {1.0, 0.82, 0.82, 0.62};
-  int best = TILE_128x128;
-  double best_cost = 1e300;
-  for (int t = 0; t < TILE_COUNT; ++t) {
-    int bm, bn;
-    gemm_tile_dims(t, &bm, &bn);
-    long tiles = 0;
-    for (int i = 0; i < np; ++i) tiles += (long)((p[i].M + bm - 1) / bm) * ((p[i].N + bn - 1) / bn);
-    const double waves = (double)((tiles + 255) / 256);
-    const double cost = waves * bm * bn / eff[t];
-    if (cost < best_cost - 1e-9) {
-      best_cost = cost;
-      best = t;
-    }
+  long t128 = 0, t64 = 0, kmax = 0;
+  for (int i = 0; i < np; ++i) {
+    t128 += (long)((p[i].M + 127) / 128) * ((p[i].N + 127) / 128);
+    t64 += (long)((p[i].M + 63) / 64) * ((p[i].N + 63) / 64);
+    kmax = p[i].K > kmax ? p[i].K : kmax;
   }
-  return best;
+  if (t128 >= 192 || kmax >= 2048) return TILE_128x128;
+  return t64 <= 1024 ? TILE_64x64 : TILE_64x128;
 }
 
 hipError_t run_gemm(Gemm& G, int dtype, hipStream_t st) {
@@ -341,7 +334,7 @@ dit_status run_block(const dit_shape* s, const Layout& L, char* ws, StreamIO* io
   // (7) x += gate2 * (g W_2^T + b_2)
   {
     Gemm G;
-    G.epi = EPI_RESID;
+    G.epi = EPI_RESID2;
     G.kclass = DIT_K_GEMM_FC2;
     G.a.nprob = ns;
     for (int i = 0; i < ns; ++i) {
@@ -457,8 +450,9 @@ dit_status dit_step_forward(const dit_shape* s, const dit_step_weights* w, const
   if (!w || !w->blocks) return fail(DIT_ERR_INVALID_ARG, "step weights or block array is NULL");
   if (!w->w_patch || !w->b_patch || !w->w_ada_final || !w->b_ada_final || !w->w_final || !w->b_final)
     return fail(DIT_ERR_INVALID_ARG, "a step weight pointer is NULL");
-  if (!aligned(w->w_ada_final, 16) || !aligned(w->w_final, 16) || !aligned(w->w_patch, 4))
-    return fail(DIT_ERR_INVALID_ARG, "step weight matrix misaligned");
+  if (!aligned(w->w_ada_final, 16) || !aligned(w->w_final, 16) || !aligned(w->w_patch, 4) ||
+      !aligned(w->b_final, 16))
+    return fail(DIT_ERR_INVALID_ARG, "step weight misaligned (matrices and b_final need 16 bytes)");
   if (w->pos && !aligned(w->pos, 4)) return fail(DIT_ERR_INVALID_ARG, "pos misaligned");
   const bool joint = s->text_tokens > 0;
   for (int l = 0; l < s->n_blocks; ++l) {
@@ -469,7 +463,7 @@ dit_status dit_step_forward(const dit_shape* s, const dit_step_weights* w, const
   if (joint && (!x_txt || !aligned(x_txt, 16))) return fail(DIT_ERR_INVALID_ARG, "x_txt NULL or not 16-byte aligned");
   if (!joint && x_txt) return fail(DIT_ERR_INVALID_ARG, "x_txt must be NULL when text_tokens == 0");
   if (!cond || !aligned(cond, 4)) return fail(DIT_ERR_INVALID_ARG, "cond NULL or misaligned");
-  if (!out || !aligned(out, 4)) return fail(DIT_ERR_INVALID_ARG, "out NULL or misaligned");
+  if (!out || !aligned(out, 16)) return fail(DIT_ERR_INVALID_ARG, "out NULL or not 16-byte aligned");
   const Layout L = layout(s, DIT_WS_STEP);
   if (!workspace || !aligned(workspace, 256)) return fail(DIT_ERR_INVALID_ARG, "workspace NULL or not 256-byte aligned");
   if (ws_bytes < L.total) return fail(DIT_ERR_WORKSPACE, "workspace %zu bytes < %zu needed", ws_bytes, L.total);

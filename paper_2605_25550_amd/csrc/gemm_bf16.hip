@@ -1,41 +1,75 @@
 // bf16 MFMA GEMM for the DiT block's linear layers (QKV, output projection,
 // MLP fc1/fc2 and the final layer) on gfx950:
 //   y[M, N] = A[M, K] * W[N, K]^T + bias,  fp32 accumulate,
-// followed by a fused epilogue (kernels.h: Epi).  Both operands are
-// K-contiguous, so every lane of a v_mfma_f32_32x32x16_bf16 reads 8
-// consecutive bf16 (16 bytes) of one row from LDS.
+// followed by a fused epilogue (kernels.h: Epi).
 //
-// Tiling: BM x BN x 64 per workgroup of 4 waves (2 x 2), each wave owns a
-// (BM/2) x (BN/2) sub-tile of 32x32 accumulators.  Global -> VGPR -> LDS
-// staging with two LDS buffers: the next K slice is fetched from HBM while
-// the current one feeds the matrix cores; one barrier per K slice.  LDS rows
-// carry 16 bytes of padding so the 32 rows read by a half-wavefront hit
-// distinct banks.  Workgroup ids are remapped so that neighbouring tiles
-// (which share A rows) run on the same XCD and its L2.
+// Both operands are K-contiguous.  A workgroup of 4 waves (2 x 2) owns a
+// BM x BN tile; each wave owns (BM/2) x (BN/2) as 32x32 accumulators of
+// v_mfma_f32_32x32x16_bf16, whose lanes each read 8 consecutive bf16 of one
+// row from LDS.
+//
+// Memory pipeline.  K is consumed in 32-wide slices.  Each slice of A and W
+// is copied HBM -> LDS by the global_load_lds_dwordx4 DMA path (no VGPR
+// staging, no ds_write instructions), into a ring of STAGES slice buffers;
+// STAGES-1 slices are in flight while one is consumed, so the load latency is
+// covered by STAGES-1 slices of MFMA work.  The DMA writes 16 bytes per lane
+// at consecutive LDS addresses, so rows cannot be padded; instead the 16-byte
+// chunk c of row r is stored at chunk position c ^ ((r >> 2) & 3), which
+// spreads the 16 rows read by a quarter-wavefront over distinct banks.
+// The compiler does not see the DMA (it is issued by inline assembly), so
+// the vmcnt waits that order it are explicit.
+//
+// Workgroup ids are remapped so that consecutive tiles (sharing A rows) run
+// on the same XCD and its L2.  The epilogue stages 32-row slabs of the
+// accumulators through LDS so that every global access is a contiguous 8- or
+// 16-byte vector per lane.
 #include "common.h"
 #include "kernels.h"
 
 namespace ditmi {
 
-template <int BM, int BN>
+template <int BM, int BN, int STAGES>
 struct GemmCfg {
-  static constexpr int BK = 64;
-  static constexpr int LDK = BK + 8;  // bf16 per LDS row
+  static constexpr int BK = 32;                 // K per slice (64 bytes per row)
   static constexpr int WTM = BM / 2, WTN = BN / 2;
   static constexpr int TM = WTM / 32, TN = WTN / 32;
-  static constexpr int A_CH = BM * BK / 8 / 256;  // 16-byte chunks per thread
-  static constexpr int B_CH = BN * BK / 8 / 256;
+  static constexpr int ROWS = BM + BN;          // A rows then W rows in a slice buffer
+  static constexpr int SLICE = ROWS * BK * 2;   // bytes per slice buffer
+  static constexpr int IPW = ROWS / 16 / 4;     // DMA instructions per wave per slice (16 rows each)
+  static constexpr int CST = WTN + 4;           // fp32 row stride of an epilogue slab
+  static constexpr int LDS_MAIN = STAGES * SLICE;
+  static constexpr int LDS_EPI = 4 * 32 * CST * 4;
+  static constexpr int LDS = LDS_MAIN > LDS_EPI ? LDS_MAIN : LDS_EPI;
+  static_assert(ROWS % 64 == 0, "rows must split into 16-row DMA blocks over 4 waves");
 };
 
-template <int BM, int BN, int EPI>
+__device__ __forceinline__ unsigned lds_address(const void* p) {
+  return (unsigned)(size_t)(const __attribute__((address_space(3))) void*)p;
+}
+
+// One 16-byte-per-lane DMA from global memory into LDS at (wave-uniform)
+// base + 16 * lane.
+__device__ __forceinline__ void dma_16(const void* gsrc, unsigned lds_base) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off"
+               :
+               : "s"(lds_base), "v"(gsrc)
+               : "memory", "m0");
+}
+
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  asm volatile("s_waitcnt vmcnt(%0)" : : "n"(N) : "memory");
+}
+
+template <int BM, int BN, int STAGES, int EPI>
 __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs args) {
-  using C = GemmCfg<BM, BN>;
-  __shared__ __attribute__((aligned(16))) bf16_t As[2][BM * C::LDK];
-  __shared__ __attribute__((aligned(16))) bf16_t Bs[2][BN * C::LDK];
+  using C = GemmCfg<BM, BN, STAGES>;
+  __shared__ __attribute__((aligned(1024))) unsigned char smem[C::LDS];
 
   const int tile = xcd_remap(blockIdx.x, args.total_tiles);
-  // Select the problem field by field: indexing the by-value argument array
-  // with a runtime index would copy it to scratch memory.
+  // Select the problem by value: indexing the by-value argument array with a
+  // runtime index would copy it to scratch memory.
   const bool second = args.nprob > 1 && tile >= args.p[1].tile_begin;
   const GemmProb P = second ? args.p[1] : args.p[0];
   const int local = tile - P.tile_begin;
@@ -51,40 +85,47 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs args) {
   const bf16_t* __restrict__ A = (const bf16_t*)P.A;
   const bf16_t* __restrict__ W = (const bf16_t*)P.W;
   const int M = P.M, N = P.N, K = P.K;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform (scalar) index
   const int wm = wave >> 1, wn = wave & 1;
   const int r32 = lane & 31, g = lane >> 5;
+  const unsigned lds0 = __builtin_amdgcn_readfirstlane(lds_address(smem));
 
-  const bf16_t* a_src[C::A_CH];
-  int a_dst[C::A_CH];
+  // DMA sources of this lane: block q = wave + 4t covers slice rows 16q..16q+15;
+  // lane -> row 16q + lane/4, stored chunk lane%4, fetched chunk (lane%4) ^ ((lane/16)&3).
+  const bf16_t* src[C::IPW];
 #pragma unroll
-  for (int i = 0; i < C::A_CH; ++i) {
-    int c = tid + 256 * i, row = c >> 3, kc = c & 7;
-    int grow = min(m0 + row, M - 1);
-    a_src[i] = A + (long)grow * K + kc * 8;
-    a_dst[i] = row * C::LDK + kc * 8;
+  for (int t = 0; t < C::IPW; ++t) {
+    const int q = wave + 4 * t;
+    const int row = q * 16 + (lane >> 2);
+    const int chunk = (lane & 3) ^ ((lane >> 4) & 3);
+    src[t] = row < BM ? A + (long)min(m0 + row, M - 1) * K + chunk * 8
+                      : W + (long)min(n0 + row - BM, N - 1) * K + chunk * 8;
   }
-  const bf16_t* b_src[C::B_CH];
-  int b_dst[C::B_CH];
+  const int KT = K / C::BK;
+  auto issue = [&](int slice) {  // slice index may run past the end: clamped re-read
+    const int k0 = min(slice, KT - 1) * C::BK;
+    const unsigned base = lds0 + (unsigned)((slice % STAGES) * C::SLICE);
 #pragma unroll
-  for (int i = 0; i < C::B_CH; ++i) {
-    int c = tid + 256 * i, row = c >> 3, kc = c & 7;
-    int grow = min(n0 + row, N - 1);
-    b_src[i] = W + (long)grow * K + kc * 8;
-    b_dst[i] = row * C::LDK + kc * 8;
-  }
+    for (int t = 0; t < C::IPW; ++t) dma_16(src[t] + k0, base + (unsigned)((wave + 4 * t) * 1024));
+  };
 
-  uint4 ra[C::A_CH], rb[C::B_CH];
-#define GEMM_GLOAD(k0)                                                                \
-  do {                                                                               \
-    _Pragma("unroll") for (int i = 0; i < C::A_CH; ++i) ra[i] = *(const uint4*)(a_src[i] + (k0)); \
-    _Pragma("unroll") for (int i = 0; i < C::B_CH; ++i) rb[i] = *(const uint4*)(b_src[i] + (k0)); \
-  } while (0)
-#define GEMM_LSTORE(buf)                                                              \
-  do {                                                                               \
-    _Pragma("unroll") for (int i = 0; i < C::A_CH; ++i) *(uint4*)&As[buf][a_dst[i]] = ra[i]; \
-    _Pragma("unroll") for (int i = 0; i < C::B_CH; ++i) *(uint4*)&Bs[buf][b_dst[i]] = rb[i]; \
-  } while (0)
+  // LDS read offsets of this lane's fragments within a slice buffer, per k-step s.
+  int a_off[2][C::TM], b_off[2][C::TN];
+#pragma unroll
+  for (int s = 0; s < 2; ++s) {
+    const int c = s * 2 + g;
+#pragma unroll
+    for (int i = 0; i < C::TM; ++i) {
+      const int R = wm * C::WTM + i * 32 + r32;
+      a_off[s][i] = R * 64 + ((c ^ ((R >> 2) & 3)) << 4);
+    }
+#pragma unroll
+    for (int j = 0; j < C::TN; ++j) {
+      const int R = BM + wn * C::WTN + j * 32 + r32;
+      b_off[s][j] = R * 64 + ((c ^ ((R >> 2) & 3)) << 4);
+    }
+  }
 
   f32x16 acc[C::TM][C::TN];
 #pragma unroll
@@ -92,111 +133,125 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs args) {
 #pragma unroll
     for (int j = 0; j < C::TN; ++j) acc[i][j] = f32x16{};
 
-#define GEMM_COMPUTE(buf)                                                                            \
-  do {                                                                                              \
-    _Pragma("unroll") for (int kk = 0; kk < C::BK / 16; ++kk) {                                     \
-      bf16x8 af[C::TM], bw[C::TN];                                                                  \
-      _Pragma("unroll") for (int i = 0; i < C::TM; ++i)                                             \
-        af[i] = *(const bf16x8*)&As[buf][(wm * C::WTM + i * 32 + r32) * C::LDK + kk * 16 + g * 8];  \
-      _Pragma("unroll") for (int j = 0; j < C::TN; ++j)                                             \
-        bw[j] = *(const bf16x8*)&Bs[buf][(wn * C::WTN + j * 32 + r32) * C::LDK + kk * 16 + g * 8];  \
-      _Pragma("unroll") for (int i = 0; i < C::TM; ++i)                                             \
-        _Pragma("unroll") for (int j = 0; j < C::TN; ++j)                                           \
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bw[j], acc[i][j], 0, 0, 0);    \
-    }                                                                                               \
+  // Software pipeline over slices (2 MFMA k-steps each).  Entering iteration
+  // kt, the k-step-0 fragments of slice kt are already in registers.  The
+  // k-step-1 fragments are read, the k-step-0 MFMAs issue, and while they run
+  // the wave waits for slice kt+1 and the workgroup barrier (which also frees
+  // slot kt-1 for the next DMA); then slice kt+1's k-step-0 fragments are read
+  // under the k-step-1 MFMAs.
+  static_assert(STAGES >= 4, "two slices resident plus at least one in flight");
+  bf16x8 fa0[C::TM], fb0[C::TN], fa1[C::TM], fb1[C::TN];
+#define GEMM_READ(FA, FB, slot, s)                                                            \
+  do {                                                                                       \
+    const unsigned char* b_ = smem + (slot) * C::SLICE;                                      \
+    _Pragma("unroll") for (int i = 0; i < C::TM; ++i) FA[i] = *(const bf16x8*)(b_ + a_off[s][i]); \
+    _Pragma("unroll") for (int j = 0; j < C::TN; ++j) FB[j] = *(const bf16x8*)(b_ + b_off[s][j]); \
   } while (0)
+#define GEMM_MFMA(FA, FB)                                                                     \
+  _Pragma("unroll") for (int i = 0; i < C::TM; ++i) _Pragma("unroll") for (int j = 0; j < C::TN; ++j) \
+    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(FA[i], FB[j], acc[i][j], 0, 0, 0);
 
-  // The last K slice is peeled so the prefetch in the steady-state loop is
-  // unconditional (a conditional prefetch makes the compiler keep the staging
-  // registers in scratch memory).
-  const int KT = K / C::BK;
-  GEMM_GLOAD(0);
-  GEMM_LSTORE(0);
+#pragma unroll
+  for (int s = 0; s < STAGES - 1; ++s) issue(s);
+  wait_vmcnt<(STAGES - 2) * C::IPW>();
   __syncthreads();
-  for (int kt = 0; kt + 1 < KT; ++kt) {
-    const int buf = kt & 1;
-    GEMM_GLOAD((kt + 1) * C::BK);
-    GEMM_COMPUTE(buf);
-    GEMM_LSTORE(buf ^ 1);
-    __syncthreads();
+  GEMM_READ(fa0, fb0, 0, 0);
+  int slot = 0;
+  for (int kt = 0; kt < KT; ++kt) {
+    const int next = slot + 1 == STAGES ? 0 : slot + 1;
+    GEMM_READ(fa1, fb1, slot, 1);
+    GEMM_MFMA(fa0, fb0);
+    wait_vmcnt<(STAGES - 3) * C::IPW>();  // this wave's DMA of slice kt+1 has landed
+    __syncthreads();                      // ... every wave's; slot of slice kt-1 is free
+    issue(kt + STAGES - 1);
+    GEMM_READ(fa0, fb0, next, 0);         // past the last slice this reads stale data, unused
+    GEMM_MFMA(fa1, fb1);
+    slot = next;
   }
-  GEMM_COMPUTE((KT - 1) & 1);
-#undef GEMM_COMPUTE
-#undef GEMM_GLOAD
-#undef GEMM_LSTORE
+#undef GEMM_READ
+#undef GEMM_MFMA
+  wait_vmcnt<0>();  // the clamped re-reads past the end still target LDS
 
   // ---------------------------------------------------------------- epilogue
-  // Lane holds column n = (wave col) + j*32 + r32 and rows 8*jj + 4*g + ii.
+  // Per 32-row slab i: each wave writes its 32 x (BN/2) accumulators to its
+  // own LDS region (column r32 + 32j, rows 8*jj + 4*g + ii), then reads them
+  // back four columns (or, for v^T, four rows) per lane.
   const bf16_t* __restrict__ bias = (const bf16_t*)P.bias;
-  float bn[C::TN];
-  int ncol[C::TN];
-#pragma unroll
-  for (int j = 0; j < C::TN; ++j) {
-    int n = n0 + wn * C::WTN + j * 32 + r32;
-    ncol[j] = n;
-    bn[j] = n < N ? bf2f(bias[n]) : 0.f;
-  }
-  // EPI_QKV: per-column destination (which tensor, head, d)
-  int qs[C::TN], qh[C::TN], qd[C::TN];
-  if (EPI == EPI_QKV) {
-#pragma unroll
-    for (int j = 0; j < C::TN; ++j) {
-      int n = ncol[j];
-      int s = n / P.hidden, rem = n - s * P.hidden;
-      qs[j] = s;
-      qh[j] = rem / P.head_dim;
-      qd[j] = rem - qh[j] * P.head_dim;
-    }
-  }
   const int rpb = P.rows_per_batch;
+  float* const Cw = reinterpret_cast<float*>(smem) + wave * 32 * C::CST;
+  const int nw0 = n0 + wn * C::WTN;
+  const bool vcols = EPI == EPI_QKV && n0 >= 2 * P.hidden;  // tiles never straddle k|v (2D % 128 == 0)
+  constexpr int PER_LANE = 32 * C::WTN / 4 / 64;               // 4-element groups per lane per slab
 #pragma unroll
   for (int i = 0; i < C::TM; ++i) {
+    __syncthreads();
 #pragma unroll
-    for (int jj = 0; jj < 4; ++jj) {
+    for (int j = 0; j < C::TN; ++j)
 #pragma unroll
-      for (int ii = 0; ii < 4; ++ii) {
-        const int m = m0 + wm * C::WTM + i * 32 + jj * 8 + g * 4 + ii;
-        if (m >= M) continue;
-        const int b = m / rpb;
-        const int e = jj * 4 + ii;
-        if (EPI == EPI_RESID) {
-          float* __restrict__ xr = P.resid + (long)m * N;
-          const float* __restrict__ gr = P.gate + (long)b * P.gate_stride;
+      for (int jj = 0; jj < 4; ++jj)
 #pragma unroll
-          for (int j = 0; j < C::TN; ++j) {
-            int n = ncol[j];
-            if (n < N) xr[n] = xr[n] + gr[n] * (acc[i][j][e] + bn[j]);
-          }
-        } else if (EPI == EPI_GELU) {
-          bf16_t* __restrict__ orow = (bf16_t*)P.out + (long)m * N;
+        for (int ii = 0; ii < 4; ++ii) Cw[(jj * 8 + g * 4 + ii) * C::CST + j * 32 + r32] = acc[i][j][jj * 4 + ii];
+    __syncthreads();
+    const int mb = m0 + wm * C::WTM + i * 32;
+    if (vcols) {
+      // v^T[b][h][d][j]: lane takes one column and four consecutive rows.
+      const int D = P.hidden, dh = P.head_dim;
 #pragma unroll
-          for (int j = 0; j < C::TN; ++j) {
-            int n = ncol[j];
-            if (n < N) orow[n] = f2bf(gelu_tanh(acc[i][j][e] + bn[j]));
-          }
-        } else if (EPI == EPI_STORE) {
-          float* __restrict__ orow = (float*)P.out + (long)m * N;
-#pragma unroll
-          for (int j = 0; j < C::TN; ++j) {
-            int n = ncol[j];
-            if (n < N) orow[n] = acc[i][j][e] + bn[j];
-          }
-        } else {  // EPI_QKV
-          const int jpos = m - b * rpb + P.seq_off;
-#pragma unroll
-          for (int j = 0; j < C::TN; ++j) {
-            int n = ncol[j];
-            if (n >= N) continue;
-            bf16_t val = f2bf(acc[i][j][e] + bn[j]);
-            long bh = (long)b * P.heads + qh[j];
-            if (qs[j] == 0)
-              ((bf16_t*)P.q)[(bh * P.Tj + jpos) * P.head_dim + qd[j]] = val;
-            else if (qs[j] == 1)
-              ((bf16_t*)P.k)[(bh * P.Tj + jpos) * P.head_dim + qd[j]] = val;
-            else
-              ((bf16_t*)P.v)[(bh * P.head_dim + qd[j]) * P.Tj_pad + jpos] = val;
+      for (int it = 0; it < PER_LANE; ++it) {
+        const int c = lane + 64 * it;
+        const int col = c >> 3, r4 = (c & 7) * 4;
+        const int n = nw0 + col, m = mb + r4;
+        if (n >= N || m >= M) continue;
+        const int rem = n - 2 * D, h = rem / dh, d = rem - h * dh;
+        const float bv = bf2f(bias[n]);
+        const int b = m / rpb, jp = m - b * rpb + P.seq_off;
+        const float v0 = Cw[(r4 + 0) * C::CST + col] + bv, v1 = Cw[(r4 + 1) * C::CST + col] + bv;
+        const float v2 = Cw[(r4 + 2) * C::CST + col] + bv, v3 = Cw[(r4 + 3) * C::CST + col] + bv;
+        if (m + 3 < M && (m + 3) / rpb == b && (jp & 3) == 0) {
+          bf16_t* vt = (bf16_t*)P.v + (((long)b * P.heads + h) * dh + d) * P.Tj_pad + jp;
+          *(u32x2*)vt = u32x2{pack_bf16x2(v0, v1), pack_bf16x2(v2, v3)};
+        } else {
+          const float vv[4] = {v0, v1, v2, v3};
+          for (int e = 0; e < 4 && m + e < M; ++e) {
+            const int be = (m + e) / rpb, je = (m + e) - be * rpb + P.seq_off;
+            ((bf16_t*)P.v)[(((long)be * P.heads + h) * dh + d) * P.Tj_pad + je] = f2bf(vv[e]);
           }
         }
+      }
+      continue;
+    }
+    constexpr int CPR = C::WTN / 4;  // 4-column groups per slab row
+#pragma unroll
+    for (int it = 0; it < PER_LANE; ++it) {
+      const int c = lane + 64 * it;
+      const int row = c / CPR, c4 = (c % CPR) * 4;
+      const int m = mb + row, n = nw0 + c4;
+      if (m >= M || n >= N) continue;  // N is a multiple of 4
+      const f32x4 y = *(const f32x4*)&Cw[row * C::CST + c4];
+      const u32x2 bw2 = *(const u32x2*)(bias + n);
+      const float y0 = y[0] + __uint_as_float(bw2[0] << 16), y1 = y[1] + __uint_as_float(bw2[0] & 0xFFFF0000u);
+      const float y2 = y[2] + __uint_as_float(bw2[1] << 16), y3 = y[3] + __uint_as_float(bw2[1] & 0xFFFF0000u);
+      if (EPI == EPI_RESID || EPI == EPI_RESID2) {
+        const int b = m / rpb;
+        f32x4* xr = (f32x4*)(P.resid + (long)m * N + n);
+        const f32x4 gt = *(const f32x4*)(P.gate + (long)b * P.gate_stride + n);
+        f32x4 xv = *xr;
+        xv[0] += gt[0] * y0;
+        xv[1] += gt[1] * y1;
+        xv[2] += gt[2] * y2;
+        xv[3] += gt[3] * y3;
+        *xr = xv;
+      } else if (EPI == EPI_GELU) {
+        *(u32x2*)((bf16_t*)P.out + (long)m * N + n) =
+            u32x2{pack_bf16x2(gelu_tanh(y0), gelu_tanh(y1)), pack_bf16x2(gelu_tanh(y2), gelu_tanh(y3))};
+      } else if (EPI == EPI_STORE) {
+        *(f32x4*)((float*)P.out + (long)m * N + n) = f32x4{y0, y1, y2, y3};
+      } else {  // EPI_QKV, q and k columns: 4 consecutive d of one head
+        const int D = P.hidden, dh = P.head_dim;
+        const int s = n / D, rem = n - s * D, h = rem / dh, d = rem - h * dh;
+        const int b = m / rpb, jp = m - b * rpb + P.seq_off;
+        bf16_t* dst = (bf16_t*)(s == 0 ? P.q : P.k) + (((long)b * P.heads + h) * P.Tj + jp) * dh + d;
+        *(u32x2*)dst = u32x2{pack_bf16x2(y0, y1), pack_bf16x2(y2, y3)};
       }
     }
   }
@@ -211,24 +266,25 @@ void gemm_tile_dims(int tile_cfg, int* bm, int* bn) {
   }
 }
 
-template <int BM, int BN>
+template <int BM, int BN, int STAGES>
 static hipError_t launch_tile(const GemmArgs& a, int epi, hipStream_t st) {
   dim3 grid(a.total_tiles), block(256);
   switch (epi) {
-    case EPI_QKV: hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, EPI_QKV>), grid, block, 0, st, a); break;
-    case EPI_GELU: hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, EPI_GELU>), grid, block, 0, st, a); break;
-    case EPI_RESID: hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, EPI_RESID>), grid, block, 0, st, a); break;
-    default: hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, EPI_STORE>), grid, block, 0, st, a); break;
+    case EPI_QKV: hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, STAGES, EPI_QKV>), grid, block, 0, st, a); break;
+    case EPI_GELU: hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, STAGES, EPI_GELU>), grid, block, 0, st, a); break;
+    case EPI_RESID: hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, STAGES, EPI_RESID>), grid, block, 0, st, a); break;
+    case EPI_RESID2: hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, STAGES, EPI_RESID2>), grid, block, 0, st, a); break;
+    default: hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, STAGES, EPI_STORE>), grid, block, 0, st, a); break;
   }
   return hipGetLastError();
 }
 
 hipError_t launch_gemm_bf16(const GemmArgs& a, int epi, int tile_cfg, hipStream_t st) {
   switch (tile_cfg) {
-    case TILE_64x128: return launch_tile<64, 128>(a, epi, st);
-    case TILE_128x64: return launch_tile<128, 64>(a, epi, st);
-    case TILE_64x64: return launch_tile<64, 64>(a, epi, st);
-    default: return launch_tile<128, 128>(a, epi, st);
+    case TILE_64x128: return launch_tile<64, 128, 4>(a, epi, st);
+    case TILE_128x64: return launch_tile<128, 64, 4>(a, epi, st);
+    case TILE_64x64: return launch_tile<64, 64, 4>(a, epi, st);
+    default: return launch_tile<128, 128, 4>(a, epi, st);
   }
 }
 

@@ -61,7 +61,7 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs args) {
       const int n = n0 + tx * 4 + j;
       if (n >= N) continue;
       const float y = acc[i][j] + bias[n];
-      if (EPI == EPI_RESID) {
+      if (EPI == EPI_RESID || EPI == EPI_RESID2) {
         float* xr = P.resid + (long)m * N + n;
         *xr = *xr + P.gate[(long)b * P.gate_stride + n] * y;
       } else if (EPI == EPI_GELU) {
@@ -85,6 +85,7 @@ hipError_t launch_gemm_f32(const GemmArgs& a, int epi, hipStream_t st) {
     case EPI_QKV: hipLaunchKernelGGL((gemm_f32_kernel<EPI_QKV>), grid, block, 0, st, a); break;
     case EPI_GELU: hipLaunchKernelGGL((gemm_f32_kernel<EPI_GELU>), grid, block, 0, st, a); break;
     case EPI_RESID: hipLaunchKernelGGL((gemm_f32_kernel<EPI_RESID>), grid, block, 0, st, a); break;
+    case EPI_RESID2: hipLaunchKernelGGL((gemm_f32_kernel<EPI_RESID2>), grid, block, 0, st, a); break;
     default: hipLaunchKernelGGL((gemm_f32_kernel<EPI_STORE>), grid, block, 0, st, a); break;
   }
   return hipGetLastError();

@@ -12,7 +12,9 @@ enum Epi {
   EPI_QKV = 0,    // +bias; scatter into head-major q, k and (bf16: transposed) v
   EPI_GELU = 1,   // +bias; tanh-GELU; store in the operand type
   EPI_RESID = 2,  // +bias; resid[m, n] += gate[b, n] * y   (fp32 residual stream)
-  EPI_STORE = 3   // +bias; store fp32
+  EPI_STORE = 3,  // +bias; store fp32
+  EPI_RESID2 = 4  // as EPI_RESID; a separate instantiation so the MLP's second
+                  // GEMM is a distinct kernel symbol in profiles
 };
 
 struct GemmProb {
