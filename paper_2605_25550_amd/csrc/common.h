@@ -41,6 +41,19 @@ __device__ __forceinline__ float warp_sum(float v) {
 // Value held by lane (l ^ 32): the other half of a 64-wide wavefront.
 __device__ __forceinline__ float other_half(float v) { return __shfl_xor(v, 32, 64); }
 
+// max / sum of v over lanes l and l ^ 32.  v_permlane32_swap exchanges the
+// upper half of its first operand with the lower half of its second; with
+// both operands v, the two results are {own, partner} in some order, which is
+// all a symmetric combine needs.
+__device__ __forceinline__ float max_halves(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float sum_halves(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
 // tanh-approximated GELU; tanh(z) = 1 - 2 / (exp(2z) + 1).
 __device__ __forceinline__ float gelu_tanh(float u) {
   const float k0 = 0.7978845608028654f;  // sqrt(2/pi)
@@ -58,6 +71,27 @@ __device__ __forceinline__ int xcd_remap(int i, int n) {
   int q = n / X, r = n % X;
   int xcd = i % X, idx = i / X;
   return xcd < r ? xcd * (q + 1) + idx : r * (q + 1) + (xcd - r) * q + idx;
+}
+
+// ---------------------------------------------------------------- LDS DMA
+// 32-bit LDS address of a __shared__ object.
+__device__ __forceinline__ unsigned lds_address(const void* p) {
+  return (unsigned)(size_t)(const __attribute__((address_space(3))) void*)p;
+}
+
+// One 16-byte-per-lane DMA from global memory into LDS at (wave-uniform)
+// base + 16 * lane.
+__device__ __forceinline__ void dma_16(const void* gsrc, unsigned lds_base) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off"
+               :
+               : "s"(lds_base), "v"(gsrc)
+               : "memory", "m0");
+}
+
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  asm volatile("s_waitcnt vmcnt(%0)" : : "n"(N) : "memory");
 }
 
 }  // namespace ditmi

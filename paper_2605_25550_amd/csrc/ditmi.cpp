@@ -69,6 +69,7 @@ dit_status check_shape(const dit_shape* s, bool step) {
 
 struct Layout {
   size_t mod, h, q, k, v, o, g, x, feat, h1, total;
+  size_t qk;  // q/k row length (elements)
   int ns, Tj, Tj_pad;
 };
 
@@ -96,8 +97,9 @@ Layout layout(const dit_shape* s, int kind) {
   const size_t nmod = kind == DIT_WS_STEP ? (size_t)s->n_blocks * L.ns * B * 6 * D + B * 2 * D : L.ns * B * 6 * D;
   L.mod = take(nmod * 4);
   L.h = take(rows * D * E);
-  L.q = take(B * H * L.Tj * dh * E);
-  L.k = take(B * H * L.Tj * dh * E);
+  L.qk = E == 2 ? (dh + 15) / 16 * 16 : dh;  // bf16 q/k rows are zero padded to whole MFMA k-steps
+  L.q = take(B * H * L.Tj * L.qk * E);
+  L.k = take(B * H * L.Tj * L.qk * E);
   L.v = take(E == 2 ? B * H * dh * (size_t)L.Tj_pad * 2 : B * H * L.Tj * dh * 4);
   L.o = take(rows * D * E);
   L.g = take(rows * F * E);
@@ -270,6 +272,7 @@ dit_status run_block(const dit_shape* s, const Layout& L, char* ws, StreamIO* io
       p.heads = H;
       p.head_dim = dh;
       p.hidden = D;
+      p.qk_stride = (int)L.qk;
     }
     G.flops = 2.0 * tokens * 3 * D * D;
     G.bytes = (tokens * D + ns * 3.0 * D * D + tokens * 3 * D) * E;

@@ -43,25 +43,6 @@ struct GemmCfg {
   static_assert(ROWS % 64 == 0, "rows must split into 16-row DMA blocks over 4 waves");
 };
 
-__device__ __forceinline__ unsigned lds_address(const void* p) {
-  return (unsigned)(size_t)(const __attribute__((address_space(3))) void*)p;
-}
-
-// One 16-byte-per-lane DMA from global memory into LDS at (wave-uniform)
-// base + 16 * lane.
-__device__ __forceinline__ void dma_16(const void* gsrc, unsigned lds_base) {
-  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off"
-               :
-               : "s"(lds_base), "v"(gsrc)
-               : "memory", "m0");
-}
-
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  asm volatile("s_waitcnt vmcnt(%0)" : : "n"(N) : "memory");
-}
-
 template <int BM, int BN, int STAGES, int EPI>
 __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs args) {
   using C = GemmCfg<BM, BN, STAGES>;
@@ -250,8 +231,10 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs args) {
         const int D = P.hidden, dh = P.head_dim;
         const int s = n / D, rem = n - s * D, h = rem / dh, d = rem - h * dh;
         const int b = m / rpb, jp = m - b * rpb + P.seq_off;
-        bf16_t* dst = (bf16_t*)(s == 0 ? P.q : P.k) + (((long)b * P.heads + h) * P.Tj + jp) * dh + d;
+        bf16_t* dst = (bf16_t*)(s == 0 ? P.q : P.k) + (((long)b * P.heads + h) * P.Tj + jp) * P.qk_stride + d;
         *(u32x2*)dst = u32x2{pack_bf16x2(y0, y1), pack_bf16x2(y2, y3)};
+        if (d + 4 == dh && P.qk_stride > dh)  // zero the row's padding (head_dim 72 -> 80)
+          for (int z = 4; z < P.qk_stride - dh + 4; z += 4) *(u32x2*)(dst + z) = u32x2{0u, 0u};
       }
     }
   }

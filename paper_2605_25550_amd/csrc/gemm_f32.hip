@@ -73,7 +73,8 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs args) {
         const int h = rem / P.head_dim, d = rem - h * P.head_dim;
         const int jpos = m - b * rpb + P.seq_off;
         float* dst = (float*)(s == 0 ? P.q : (s == 1 ? P.k : P.v));
-        dst[(((long)b * P.heads + h) * P.Tj + jpos) * P.head_dim + d] = y;
+        const int stride = s == 2 ? P.head_dim : P.qk_stride;
+        dst[(((long)b * P.heads + h) * P.Tj + jpos) * stride + d] = y;
       }
     }
   }

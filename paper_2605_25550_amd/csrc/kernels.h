@@ -31,10 +31,11 @@ struct GemmProb {
   // EPI_GELU / EPI_STORE
   void* out;           // [M, N] row-major
   // EPI_QKV: row m -> (b, j = m % rows_per_batch + seq_off) of the joint sequence
-  void* q;             // [B, H, Tj, dh]
-  void* k;             // [B, H, Tj, dh]
+  void* q;             // [B, H, Tj, qk_stride]
+  void* k;             // [B, H, Tj, qk_stride]
   void* v;             // bf16: v^T [B, H, dh, Tj_pad]; fp32: [B, H, Tj, dh]
   int seq_off, Tj, Tj_pad, heads, head_dim, hidden;
+  int qk_stride;       // q/k row length: head_dim, or (bf16) head_dim rounded up to 16, zero padded
 };
 
 struct GemmArgs {
@@ -45,8 +46,8 @@ struct GemmArgs {
 
 // ------------------------------------------------------------------ attention
 struct AttnArgs {
-  const void* q;   // [B, H, Tj, dh]
-  const void* k;   // [B, H, Tj, dh]
+  const void* q;   // bf16: [B, H, Tj, round16(dh)] zero padded; fp32: [B, H, Tj, dh]
+  const void* k;   // same layout as q
   const void* v;   // bf16: v^T [B, H, dh, Tj_pad]; fp32: [B, H, Tj, dh]
   void* o;         // stream-major rows: image b*T + t, then text B*T + b*Tt + t; [*, H*dh]
   int B, H, Tj, Tj_pad, T_img, T_txt, D;
