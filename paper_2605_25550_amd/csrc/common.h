@@ -38,6 +38,23 @@ __device__ __forceinline__ float warp_sum(float v) {
   return v;
 }
 
+// Sum over the 64 lanes: DPP moves combine within each 16-lane row (lane
+// pairs, quads, half-row mirror, row mirror), then the four row sums are read
+// as scalars.  No LDS-crossbar permutes; every lane receives the total.
+template <int CTRL>
+__device__ __forceinline__ float dpp_move(float x) {
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), CTRL, 0xF, 0xF, false));
+}
+__device__ __forceinline__ float wave_sum(float v) {
+  v += dpp_move<0xB1>(v);   // quad_perm [1,0,3,2]
+  v += dpp_move<0x4E>(v);   // quad_perm [2,3,0,1]
+  v += dpp_move<0x141>(v);  // row_half_mirror
+  v += dpp_move<0x140>(v);  // row_mirror: each lane holds its row's sum
+  const int b = __float_as_int(v);
+  return (__int_as_float(__builtin_amdgcn_readlane(b, 0)) + __int_as_float(__builtin_amdgcn_readlane(b, 16))) +
+         (__int_as_float(__builtin_amdgcn_readlane(b, 32)) + __int_as_float(__builtin_amdgcn_readlane(b, 48)));
+}
+
 // Value held by lane (l ^ 32): the other half of a 64-wide wavefront.
 __device__ __forceinline__ float other_half(float v) { return __shfl_xor(v, 32, 64); }
 

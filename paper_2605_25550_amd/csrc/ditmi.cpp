@@ -157,18 +157,16 @@ struct Gemm {
   double flops = 0, bytes = 0;
 };
 
-// bf16 tile choice (measured on MI355X): 128x128 tiles are the most
-// efficient per CU; when they would leave most CUs idle on a short K loop,
-// smaller tiles spread the work over more CUs.
+// bf16 tile choice (measured on MI355X, 256 CUs, two workgroups per CU):
+// 128x128 tiles are the most efficient per CU, but a launch is charged for
+// every started round of 512 tiles, so tile counts that would spill a little
+// into a second round (256..511 is one round; 512..767 is not) and counts that
+// leave most CUs idle (< 256) use 64x128 tiles instead.
 int choose_tile(const GemmProb* p, int np) {
-  long t128 = 0, t64 = 0, kmax = 0;
-  for (int i = 0; i < np; ++i) {
-    t128 += (long)((p[i].M + 127) / 128) * ((p[i].N + 127) / 128);
-    t64 += (long)((p[i].M + 63) / 64) * ((p[i].N + 63) / 64);
-    kmax = p[i].K > kmax ? p[i].K : kmax;
-  }
-  if (t128 >= 192 || kmax >= 2048) return TILE_128x128;
-  return t64 <= 1024 ? TILE_64x64 : TILE_64x128;
+  long t128 = 0;
+  for (int i = 0; i < np; ++i) t128 += (long)((p[i].M + 127) / 128) * ((p[i].N + 127) / 128);
+  const bool big = (t128 >= 256 && t128 < 512) || t128 >= 768;
+  return big ? TILE_128x128 : TILE_64x128;
 }
 
 hipError_t run_gemm(Gemm& G, int dtype, hipStream_t st) {

@@ -25,15 +25,23 @@ __global__ __launch_bounds__(256) void ln_mod_kernel(LnArgs a) {
   const int D = a.D, nq = D >> 2;
   const float4* __restrict__ xr = (const float4*)(S.x + (long)r * D);
 
-  float4 v[NV];
+  // shift/scale are loaded with x, before the reductions, so that their
+  // latency overlaps the row's.
+  const float4* __restrict__ sh = (const float4*)(S.shift + (long)b * S.mod_stride);
+  const float4* __restrict__ sc = (const float4*)(S.scale + (long)b * S.mod_stride);
+  float4 v[NV], s4[NV], c4[NV];
   float sum = 0.f;
 #pragma unroll
   for (int i = 0; i < NV; ++i) {
     const int c = lane + 64 * i;
-    v[i] = c < nq ? xr[c] : make_float4(0.f, 0.f, 0.f, 0.f);
+    const bool in = c < nq;
+    const float4 z = make_float4(0.f, 0.f, 0.f, 0.f);
+    v[i] = in ? xr[c] : z;
+    s4[i] = in ? sh[c] : z;
+    c4[i] = in ? sc[c] : z;
     sum += (v[i].x + v[i].y) + (v[i].z + v[i].w);
   }
-  const float mean = warp_sum(sum) / (float)D;
+  const float mean = wave_sum(sum) / (float)D;
   float sq = 0.f;
 #pragma unroll
   for (int i = 0; i < NV; ++i) {
@@ -43,19 +51,16 @@ __global__ __launch_bounds__(256) void ln_mod_kernel(LnArgs a) {
       sq += (dx * dx + dy * dy) + (dz * dz + dw * dw);
     }
   }
-  const float var = warp_sum(sq) / (float)D;
+  const float var = wave_sum(sq) / (float)D;
   const float rstd = 1.0f / sqrtf(var + a.eps);
-  const float4* __restrict__ sh = (const float4*)(S.shift + (long)b * S.mod_stride);
-  const float4* __restrict__ sc = (const float4*)(S.scale + (long)b * S.mod_stride);
 #pragma unroll
   for (int i = 0; i < NV; ++i) {
     const int c = lane + 64 * i;
     if (c >= nq) continue;
-    const float4 s4 = sh[c], c4 = sc[c];
-    const float y0 = (v[i].x - mean) * rstd * (1.f + c4.x) + s4.x;
-    const float y1 = (v[i].y - mean) * rstd * (1.f + c4.y) + s4.y;
-    const float y2 = (v[i].z - mean) * rstd * (1.f + c4.z) + s4.z;
-    const float y3 = (v[i].w - mean) * rstd * (1.f + c4.w) + s4.w;
+    const float y0 = (v[i].x - mean) * rstd * (1.f + c4[i].x) + s4[i].x;
+    const float y1 = (v[i].y - mean) * rstd * (1.f + c4[i].y) + s4[i].y;
+    const float y2 = (v[i].z - mean) * rstd * (1.f + c4[i].z) + s4[i].z;
+    const float y3 = (v[i].w - mean) * rstd * (1.f + c4[i].w) + s4[i].w;
     if constexpr (sizeof(OutT) == 2) {
       uint2 w = make_uint2(pack_bf16x2(y0, y1), pack_bf16x2(y2, y3));
       ((uint2*)S.out)[(long)r * nq + c] = w;

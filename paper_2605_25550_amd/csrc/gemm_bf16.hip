@@ -8,16 +8,21 @@
 // v_mfma_f32_32x32x16_bf16, whose lanes each read 8 consecutive bf16 of one
 // row from LDS.
 //
-// Memory pipeline.  K is consumed in 32-wide slices.  Each slice of A and W
-// is copied HBM -> LDS by the global_load_lds_dwordx4 DMA path (no VGPR
-// staging, no ds_write instructions), into a ring of STAGES slice buffers;
-// STAGES-1 slices are in flight while one is consumed, so the load latency is
-// covered by STAGES-1 slices of MFMA work.  The DMA writes 16 bytes per lane
-// at consecutive LDS addresses, so rows cannot be padded; instead the 16-byte
-// chunk c of row r is stored at chunk position c ^ ((r >> 2) & 3), which
-// spreads the 16 rows read by a quarter-wavefront over distinct banks.
-// The compiler does not see the DMA (it is issued by inline assembly), so
-// the vmcnt waits that order it are explicit.
+// Memory pipeline.  K is consumed in 64-wide slices (128 bytes per row, one
+// full cache line).  Each slice of A and W is copied HBM -> LDS by the
+// global_load_lds_dwordx4 DMA path (no VGPR staging, no ds_write
+// instructions) into a ring of STAGES slice buffers.  A DMA instruction moves
+// 8 rows x 128 bytes; its address is a scalar base (operand + k offset) plus a
+// fixed 32-bit per-lane offset, so the loop spends no vector ALU work on
+// addresses.  A slot is refilled as soon as every wave has read its last
+// fragments (before the last k-step's MFMAs), so STAGES - 1 slices are in
+// flight while one is consumed.  Rows cannot be padded (the DMA writes 16
+// bytes per lane at consecutive LDS addresses); instead the 16-byte chunk c
+// of row r is stored at position c ^ f(r), f(r) = (r & 7) ^ ((r >> 3) & 1),
+// which keeps the 16 rows read by one quarter-wavefront on distinct banks.
+// The compiler does not see the DMA (inline assembly), so the vmcnt waits
+// that order it are explicit, and scheduling barriers keep each k-step's
+// fragment reads one MFMA group ahead of their use.
 //
 // Workgroup ids are remapped so that consecutive tiles (sharing A rows) run
 // on the same XCD and its L2.  The epilogue stages 32-row slabs of the
@@ -30,18 +35,32 @@ namespace ditmi {
 
 template <int BM, int BN, int STAGES>
 struct GemmCfg {
-  static constexpr int BK = 32;                 // K per slice (64 bytes per row)
+  static constexpr int BK = 64;                 // K per slice (128 bytes per row)
   static constexpr int WTM = BM / 2, WTN = BN / 2;
   static constexpr int TM = WTM / 32, TN = WTN / 32;
   static constexpr int ROWS = BM + BN;          // A rows then W rows in a slice buffer
-  static constexpr int SLICE = ROWS * BK * 2;   // bytes per slice buffer
-  static constexpr int IPW = ROWS / 16 / 4;     // DMA instructions per wave per slice (16 rows each)
+  static constexpr int SLICE = ROWS * 128;      // bytes per slice buffer
+  static constexpr int IPW = ROWS / 32;         // DMA instructions (8 rows each) per wave per slice
+  static constexpr int IPW_A = BM / 32;         // ... of which read A
   static constexpr int CST = WTN + 4;           // fp32 row stride of an epilogue slab
   static constexpr int LDS_MAIN = STAGES * SLICE;
   static constexpr int LDS_EPI = 4 * 32 * CST * 4;
   static constexpr int LDS = LDS_MAIN > LDS_EPI ? LDS_MAIN : LDS_EPI;
-  static_assert(ROWS % 64 == 0, "rows must split into 16-row DMA blocks over 4 waves");
+  static_assert(BM % 64 == 0 && BN % 64 == 0, "wave tiles are multiples of 32");
+  static_assert(STAGES >= 2 && (STAGES - 1) * IPW < 64, "vmcnt range");
 };
+
+// Stored position of 16-byte chunk c of slice row r.
+__device__ __forceinline__ int chunk_pos(int r, int c) { return c ^ ((r & 7) ^ ((r >> 3) & 1)); }
+
+// 16 bytes per lane from sbase + voff (sbase wave-uniform) into LDS at
+// (wave-uniform) lds_base + 16 * lane.
+__device__ __forceinline__ void dma_16s(const void* sbase, unsigned voff, unsigned lds_base) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2"
+               :
+               : "s"(lds_base), "v"(voff), "s"(sbase)
+               : "memory", "m0");
+}
 
 template <int BM, int BN, int STAGES, int EPI>
 __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs args) {
@@ -66,45 +85,47 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs args) {
   const bf16_t* __restrict__ A = (const bf16_t*)P.A;
   const bf16_t* __restrict__ W = (const bf16_t*)P.W;
   const int M = P.M, N = P.N, K = P.K;
+  const int KT = K / C::BK;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform (scalar) index
   const int wm = wave >> 1, wn = wave & 1;
   const int r32 = lane & 31, g = lane >> 5;
   const unsigned lds0 = __builtin_amdgcn_readfirstlane(lds_address(smem));
 
-  // DMA sources of this lane: block q = wave + 4t covers slice rows 16q..16q+15;
-  // lane -> row 16q + lane/4, stored chunk lane%4, fetched chunk (lane%4) ^ ((lane/16)&3).
-  const bf16_t* src[C::IPW];
+  // DMA instruction t of this wave fills slice rows 8q .. 8q+7, q = wave + 4t;
+  // lane -> row 8q + lane/8 at stored position lane%8, which holds chunk
+  // (lane%8) ^ f(row) = (lane%8) ^ (lane/8) ^ (q&1), and q&1 = wave&1.
+  const int cfetch = (lane & 7) ^ (lane >> 3) ^ (wave & 1);
+  unsigned voff[C::IPW];
 #pragma unroll
   for (int t = 0; t < C::IPW; ++t) {
-    const int q = wave + 4 * t;
-    const int row = q * 16 + (lane >> 2);
-    const int chunk = (lane & 3) ^ ((lane >> 4) & 3);
-    src[t] = row < BM ? A + (long)min(m0 + row, M - 1) * K + chunk * 8
-                      : W + (long)min(n0 + row - BM, N - 1) * K + chunk * 8;
+    const int row = 8 * (wave + 4 * t) + (lane >> 3);
+    const int grow = t < C::IPW_A ? min(m0 + row, M - 1) : min(n0 + row - BM, N - 1);  // clamped: ragged tiles
+    voff[t] = (unsigned)grow * (unsigned)K * 2u + (unsigned)cfetch * 16u;
   }
-  const int KT = K / C::BK;
-  auto issue = [&](int slice) {  // slice index may run past the end: clamped re-read
-    const int k0 = min(slice, KT - 1) * C::BK;
-    const unsigned base = lds0 + (unsigned)((slice % STAGES) * C::SLICE);
+  auto issue = [&](int slice, int slot) {
+    const long kb = (long)slice * C::BK;
+    const bf16_t* sa = A + kb;
+    const bf16_t* sw = W + kb;
+    const unsigned base = lds0 + (unsigned)(slot * C::SLICE) + (unsigned)(wave * 1024);
 #pragma unroll
-    for (int t = 0; t < C::IPW; ++t) dma_16(src[t] + k0, base + (unsigned)((wave + 4 * t) * 1024));
+    for (int t = 0; t < C::IPW; ++t) dma_16s(t < C::IPW_A ? sa : sw, voff[t], base + (unsigned)(t * 4096));
   };
 
   // LDS read offsets of this lane's fragments within a slice buffer, per k-step s.
-  int a_off[2][C::TM], b_off[2][C::TN];
+  int a_off[4][C::TM], b_off[4][C::TN];
 #pragma unroll
-  for (int s = 0; s < 2; ++s) {
+  for (int s = 0; s < 4; ++s) {
     const int c = s * 2 + g;
 #pragma unroll
     for (int i = 0; i < C::TM; ++i) {
       const int R = wm * C::WTM + i * 32 + r32;
-      a_off[s][i] = R * 64 + ((c ^ ((R >> 2) & 3)) << 4);
+      a_off[s][i] = R * 128 + (chunk_pos(R, c) << 4);
     }
 #pragma unroll
     for (int j = 0; j < C::TN; ++j) {
       const int R = BM + wn * C::WTN + j * 32 + r32;
-      b_off[s][j] = R * 64 + ((c ^ ((R >> 2) & 3)) << 4);
+      b_off[s][j] = R * 128 + (chunk_pos(R, c) << 4);
     }
   }
 
@@ -114,14 +135,6 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs args) {
 #pragma unroll
     for (int j = 0; j < C::TN; ++j) acc[i][j] = f32x16{};
 
-  // Software pipeline over slices (2 MFMA k-steps each).  Entering iteration
-  // kt, the k-step-0 fragments of slice kt are already in registers.  The
-  // k-step-1 fragments are read, the k-step-0 MFMAs issue, and while they run
-  // the wave waits for slice kt+1 and the workgroup barrier (which also frees
-  // slot kt-1 for the next DMA); then slice kt+1's k-step-0 fragments are read
-  // under the k-step-1 MFMAs.
-  static_assert(STAGES >= 4, "two slices resident plus at least one in flight");
-  bf16x8 fa0[C::TM], fb0[C::TN], fa1[C::TM], fb1[C::TN];
 #define GEMM_READ(FA, FB, slot, s)                                                            \
   do {                                                                                       \
     const unsigned char* b_ = smem + (slot) * C::SLICE;                                      \
@@ -131,27 +144,54 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs args) {
 #define GEMM_MFMA(FA, FB)                                                                     \
   _Pragma("unroll") for (int i = 0; i < C::TM; ++i) _Pragma("unroll") for (int j = 0; j < C::TN; ++j) \
     acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(FA[i], FB[j], acc[i][j], 0, 0, 0);
+#define SCHED_FENCE() __builtin_amdgcn_sched_barrier(0)
 
+  // Slices past the end are not issued; where fewer than the steady-state
+  // number are in flight, the waits fall back to vmcnt(0).
 #pragma unroll
-  for (int s = 0; s < STAGES - 1; ++s) issue(s);
-  wait_vmcnt<(STAGES - 2) * C::IPW>();
+  for (int s = 0; s < STAGES; ++s)
+    if (s < KT) issue(s, s);
+  if (KT >= STAGES) wait_vmcnt<(STAGES - 1) * C::IPW>();
+  else wait_vmcnt<0>();
   __syncthreads();
-  GEMM_READ(fa0, fb0, 0, 0);
+
+  // Software pipeline over slices (4 MFMA k-steps each), fragments double
+  // buffered per k-step in X (even k-steps) and Y (odd).  Entering iteration
+  // kt, X holds k-step 0 of slice kt.  Each k-step's reads are issued before
+  // the previous k-step's MFMAs.  After the last reads of slot kt, the wave
+  // waits for its DMA of slice kt+1; the workgroup barrier then guarantees
+  // every wave's DMA of kt+1 has landed and every read of slot kt is
+  // complete, so slice kt+STAGES is issued into that slot.
+  bf16x8 xa[C::TM], xb[C::TN], ya[C::TM], yb[C::TN];
+  GEMM_READ(xa, xb, 0, 0);
   int slot = 0;
   for (int kt = 0; kt < KT; ++kt) {
     const int next = slot + 1 == STAGES ? 0 : slot + 1;
-    GEMM_READ(fa1, fb1, slot, 1);
-    GEMM_MFMA(fa0, fb0);
-    wait_vmcnt<(STAGES - 3) * C::IPW>();  // this wave's DMA of slice kt+1 has landed
-    __syncthreads();                      // ... every wave's; slot of slice kt-1 is free
-    issue(kt + STAGES - 1);
-    GEMM_READ(fa0, fb0, next, 0);         // past the last slice this reads stale data, unused
-    GEMM_MFMA(fa1, fb1);
+    GEMM_READ(ya, yb, slot, 1);
+    SCHED_FENCE();
+    GEMM_MFMA(xa, xb);
+    SCHED_FENCE();
+    GEMM_READ(xa, xb, slot, 2);
+    SCHED_FENCE();
+    GEMM_MFMA(ya, yb);
+    SCHED_FENCE();
+    GEMM_READ(ya, yb, slot, 3);
+    SCHED_FENCE();
+    GEMM_MFMA(xa, xb);
+    SCHED_FENCE();
+    if (kt + STAGES - 1 < KT) wait_vmcnt<(STAGES - 2) * C::IPW>();  // own DMA of slice kt+1 landed
+    else wait_vmcnt<0>();
+    __syncthreads();
+    if (kt + STAGES < KT) issue(kt + STAGES, slot);
+    GEMM_READ(xa, xb, next, 0);  // past the last slice this reads stale data, unused
+    SCHED_FENCE();
+    GEMM_MFMA(ya, yb);
+    SCHED_FENCE();
     slot = next;
   }
 #undef GEMM_READ
 #undef GEMM_MFMA
-  wait_vmcnt<0>();  // the clamped re-reads past the end still target LDS
+#undef SCHED_FENCE
 
   // ---------------------------------------------------------------- epilogue
   // Per 32-row slab i: each wave writes its 32 x (BN/2) accumulators to its
@@ -245,6 +285,9 @@ void gemm_tile_dims(int tile_cfg, int* bm, int* bn) {
     case TILE_64x128: *bm = 64; *bn = 128; break;
     case TILE_128x64: *bm = 128; *bn = 64; break;
     case TILE_64x64: *bm = 64; *bn = 64; break;
+    case TILE_256x128: *bm = 256; *bn = 128; break;
+    case TILE_128x256: *bm = 128; *bn = 256; break;
+    case TILE_256x256: *bm = 256; *bn = 256; break;
     default: *bm = 128; *bn = 128; break;
   }
 }
@@ -262,12 +305,18 @@ static hipError_t launch_tile(const GemmArgs& a, int epi, hipStream_t st) {
   return hipGetLastError();
 }
 
+// Stage counts: a slice is (BM + BN) x 128 bytes; the ring sizes below keep
+// two workgroups per CU up to 128x128 (measured faster than a deeper ring
+// with one workgroup) and fit 160 KB for the large tiles.
 hipError_t launch_gemm_bf16(const GemmArgs& a, int epi, int tile_cfg, hipStream_t st) {
   switch (tile_cfg) {
-    case TILE_64x128: return launch_tile<64, 128, 4>(a, epi, st);
-    case TILE_128x64: return launch_tile<128, 64, 4>(a, epi, st);
+    case TILE_64x128: return launch_tile<64, 128, 3>(a, epi, st);
+    case TILE_128x64: return launch_tile<128, 64, 3>(a, epi, st);
     case TILE_64x64: return launch_tile<64, 64, 4>(a, epi, st);
-    default: return launch_tile<128, 128, 4>(a, epi, st);
+    case TILE_256x128: return launch_tile<256, 128, 3>(a, epi, st);
+    case TILE_128x256: return launch_tile<128, 256, 3>(a, epi, st);
+    case TILE_256x256: return launch_tile<256, 256, 2>(a, epi, st);
+    default: return launch_tile<128, 128, 2>(a, epi, st);
   }
 }
 

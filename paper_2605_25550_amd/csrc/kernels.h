@@ -100,7 +100,10 @@ hipError_t launch_patch_embed(int rows, int T, int P, int D, const float* z, con
 hipError_t launch_pos_embed_2d(int gh, int gw, int D, float* pos, hipStream_t st);
 
 // Tile configurations of the bf16 GEMM (BM x BN).
-enum { TILE_128x128 = 0, TILE_64x128 = 1, TILE_128x64 = 2, TILE_64x64 = 3, TILE_COUNT = 4 };
+enum {
+  TILE_128x128 = 0, TILE_64x128 = 1, TILE_128x64 = 2, TILE_64x64 = 3,
+  TILE_256x128 = 4, TILE_128x256 = 5, TILE_256x256 = 6, TILE_COUNT = 7
+};
 void gemm_tile_dims(int tile_cfg, int* bm, int* bn);
 
 }  // namespace ditmi
