@@ -69,7 +69,7 @@ dit_status check_shape(const dit_shape* s, bool step) {
 }
 
 struct Layout {
-  size_t mod, h, q, k, v, o, g, x, feat, h1, total;
+  size_t mod, act, h, q, k, v, o, g, x, feat, h1, total;
   size_t qk;  // q/k row length (elements)
   int ns, Tj, Tj_pad;
 };
@@ -97,6 +97,7 @@ Layout layout(const dit_shape* s, int kind) {
   const size_t rows = B * (T + Tt);
   const size_t nmod = kind == DIT_WS_STEP ? (size_t)s->n_blocks * L.ns * B * 6 * D + B * 2 * D : L.ns * B * 6 * D;
   L.mod = take(nmod * 4);
+  L.act = take((B + 15) / 16 * 16 * D * 2);  // SiLU(c) in bf16 for the adaLN MFMA kernel
   L.h = take(rows * D * E);
   L.qk = E == 2 ? (dh + 15) / 16 * 16 : dh;  // bf16 q/k rows are zero padded to whole MFMA k-steps
   L.q = take(B * H * L.Tj * L.qk * E);
@@ -421,11 +422,15 @@ struct AdaJob {
   int N;
 };
 
-dit_status run_adaln(const dit_shape* s, const float* cond, const std::vector<AdaJob>& jobs, hipStream_t st) {
+dit_status run_adaln(const dit_shape* s, const float* cond, void* act, const std::vector<AdaJob>& jobs,
+                     hipStream_t st) {
   const size_t E = s->dtype == DIT_BF16 ? 2 : 4;
+  if (s->dtype == DIT_BF16)
+    HIP_TRY(timed(DIT_K_ADALN, 0, 0, st, [&]() { return launch_silu_bf16(s->batch, s->hidden, cond, act, st); }));
   for (size_t j0 = 0; j0 < jobs.size(); j0 += ADA_MAX_ENTRIES) {
     AdaArgs a{};
     a.cond = cond;
+    a.act = act;
     a.B = s->batch;
     a.D = s->hidden;
     int wg = 0;
@@ -500,7 +505,7 @@ dit_status dit_block_forward(const dit_shape* s, const dit_block_weights* w, flo
   std::vector<AdaJob> jobs;
   jobs.push_back({w->img.w_ada, w->img.b_ada, mod, 6 * s->hidden});
   if (joint) jobs.push_back({w->txt.w_ada, w->txt.b_ada, mod + per, 6 * s->hidden});
-  if ((st = run_adaln(s, cond, jobs, hs)) != DIT_OK) return st;
+  if ((st = run_adaln(s, cond, ws + L.act, jobs, hs)) != DIT_OK) return st;
   StreamIO io[2] = {{&w->img, x, mod, s->tokens}, {&w->txt, x_txt, mod + per, s->text_tokens}};
   return run_block(s, L, ws, io, joint ? 2 : 1, hs);
 }
@@ -545,7 +550,7 @@ dit_status dit_step_forward(const dit_shape* s, const dit_step_weights* w, const
     if (joint) jobs.push_back({w->blocks[l].txt.w_ada, w->blocks[l].txt.b_ada, mod + (size_t)(l * ns + 1) * per, 6 * D});
   }
   jobs.push_back({w->w_ada_final, w->b_ada_final, mod_final, 2 * D});
-  if ((st = run_adaln(s, cond, jobs, hs)) != DIT_OK) return st;
+  if ((st = run_adaln(s, cond, ws + L.act, jobs, hs)) != DIT_OK) return st;
 
   // (a3) x = patches W_patch^T + b_patch (+ pos)
   HIP_TRY(timed(DIT_K_OTHER, 2.0 * B * T * D * s->patch_in, (double)B * T * (s->patch_in + D) * 4.0, hs, [&]() {
@@ -603,6 +608,8 @@ dit_status dit_cond_embed(const dit_shape* s, const float* t, const int32_t* y, 
   if (st != DIT_OK) return st;
   if (!t || !y || !w_t1 || !b_t1 || !w_t2 || !b_t2 || !class_table || !cond)
     return fail(DIT_ERR_INVALID_ARG, "a conditioning pointer is NULL");
+  if (!aligned(w_t1, 16) || !aligned(w_t2, 16))
+    return fail(DIT_ERR_INVALID_ARG, "w_t1 and w_t2 must be 16-byte aligned");
   const Layout L = layout(s, DIT_WS_COND);
   if (!workspace || !aligned(workspace, 256)) return fail(DIT_ERR_INVALID_ARG, "workspace NULL or not 256-byte aligned");
   if (ws_bytes < L.total) return fail(DIT_ERR_WORKSPACE, "workspace %zu bytes < %zu needed", ws_bytes, L.total);

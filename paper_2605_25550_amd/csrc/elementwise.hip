@@ -19,37 +19,42 @@ __global__ __launch_bounds__(256) void ln_mod_kernel(LnArgs a) {
   const int lane = threadIdx.x & 63;
   if (row >= a.total_rows) return;  // whole wavefront leaves together
   const int si = (a.nseg > 1 && row >= a.s[1].row_begin) ? 1 : 0;
-  const LnSeg& S = a.s[si];
+  // select by value: indexing the by-value argument array with a runtime
+  // index would copy it to scratch memory
+  const LnSeg S = si ? a.s[1] : a.s[0];
   const int r = row - S.row_begin;
   const int b = r / S.rows_per_batch;
   const int D = a.D, nq = D >> 2;
-  const float4* __restrict__ xr = (const float4*)(S.x + (long)r * D);
+  const f32x4* __restrict__ xr = (const f32x4*)(S.x + (long)r * D);
 
   // shift/scale are loaded with x, before the reductions, so that their
-  // latency overlaps the row's.
-  const float4* __restrict__ sh = (const float4*)(S.shift + (long)b * S.mod_stride);
-  const float4* __restrict__ sc = (const float4*)(S.scale + (long)b * S.mod_stride);
-  float4 v[NV], s4[NV], c4[NV];
+  // latency overlaps the row's.  Loads use a clamped (always valid) index and
+  // the values are selected afterwards; vectors are clang ext_vector types
+  // (HIP's float4/uint2 structs, kept in arrays, are placed in memory).
+  const f32x4* __restrict__ sh = (const f32x4*)(S.shift + (long)b * S.mod_stride);
+  const f32x4* __restrict__ sc = (const f32x4*)(S.scale + (long)b * S.mod_stride);
+  f32x4 v[NV], s4[NV], c4[NV];
   float sum = 0.f;
+  const f32x4 z = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int i = 0; i < NV; ++i) {
     const int c = lane + 64 * i;
+    const int cc = min(c, nq - 1);
     const bool in = c < nq;
-    const float4 z = make_float4(0.f, 0.f, 0.f, 0.f);
-    v[i] = in ? xr[c] : z;
-    s4[i] = in ? sh[c] : z;
-    c4[i] = in ? sc[c] : z;
-    sum += (v[i].x + v[i].y) + (v[i].z + v[i].w);
+    const f32x4 tx = xr[cc], ts = sh[cc], tc = sc[cc];
+    v[i] = in ? tx : z;
+    s4[i] = in ? ts : z;
+    c4[i] = in ? tc : z;
+    sum += (v[i][0] + v[i][1]) + (v[i][2] + v[i][3]);
   }
   const float mean = wave_sum(sum) / (float)D;
   float sq = 0.f;
 #pragma unroll
   for (int i = 0; i < NV; ++i) {
     const int c = lane + 64 * i;
-    if (c < nq) {
-      const float dx = v[i].x - mean, dy = v[i].y - mean, dz = v[i].z - mean, dw = v[i].w - mean;
-      sq += (dx * dx + dy * dy) + (dz * dz + dw * dw);
-    }
+    const f32x4 d = v[i] - mean;
+    const float q = (d[0] * d[0] + d[1] * d[1]) + (d[2] * d[2] + d[3] * d[3]);
+    sq += c < nq ? q : 0.f;
   }
   const float var = wave_sum(sq) / (float)D;
   const float rstd = 1.0f / sqrtf(var + a.eps);
@@ -57,15 +62,11 @@ __global__ __launch_bounds__(256) void ln_mod_kernel(LnArgs a) {
   for (int i = 0; i < NV; ++i) {
     const int c = lane + 64 * i;
     if (c >= nq) continue;
-    const float y0 = (v[i].x - mean) * rstd * (1.f + c4[i].x) + s4[i].x;
-    const float y1 = (v[i].y - mean) * rstd * (1.f + c4[i].y) + s4[i].y;
-    const float y2 = (v[i].z - mean) * rstd * (1.f + c4[i].z) + s4[i].z;
-    const float y3 = (v[i].w - mean) * rstd * (1.f + c4[i].w) + s4[i].w;
+    const f32x4 y = (v[i] - mean) * rstd * (1.f + c4[i]) + s4[i];
     if constexpr (sizeof(OutT) == 2) {
-      uint2 w = make_uint2(pack_bf16x2(y0, y1), pack_bf16x2(y2, y3));
-      ((uint2*)S.out)[(long)r * nq + c] = w;
+      ((u32x2*)S.out)[(long)r * nq + c] = u32x2{pack_bf16x2(y[0], y[1]), pack_bf16x2(y[2], y[3])};
     } else {
-      ((float4*)S.out)[(long)r * nq + c] = make_float4(y0, y1, y2, y3);
+      ((f32x4*)S.out)[(long)r * nq + c] = y;
     }
   }
 }
@@ -190,15 +191,87 @@ __global__ __launch_bounds__(256) void adaln_kernel(AdaArgs a) {
   }
 }
 
+// bf16 weights: the same product on v_mfma_f32_16x16x32_bf16 as
+// out^T [N, B] = W [N, K] * SiLU(c)^T [K, B].  A workgroup (4 waves x 2 row
+// tiles of 16) owns 128 rows of one entry.  A-operand lanes read their 16
+// bytes of W straight from global memory (row lane%16, k offset 8*(lane/16));
+// the B operand, SiLU(c) in bf16 for 16 samples (computed once by
+// silu_bf16_kernel, zero rows past the batch), is copied to LDS with a
+// 16-byte row pad so that the 16 rows read by a quarter-wave fall on distinct
+// banks.  Batches above 16 loop over 16-sample tiles.  D lanes hold column
+// (sample) lane%16, rows 4*(lane/16) + i.
+__global__ void silu_bf16_kernel(int B, int D, int rows, const float* cond, bf16_t* act) {
+  const long idx = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= (long)rows * D) return;
+  const int r = (int)(idx / D);
+  act[idx] = r < B ? f2bf(silu(cond[idx])) : (bf16_t)0;
+}
+
+hipError_t launch_silu_bf16(int B, int D, const float* cond, void* act, hipStream_t st) {
+  const int rows = (B + 15) / 16 * 16;
+  const long n = (long)rows * D;
+  hipLaunchKernelGGL(silu_bf16_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, B, D, rows, cond,
+                     (bf16_t*)act);
+  return hipGetLastError();
+}
+
+__global__ __launch_bounds__(256) void adaln_mfma_kernel(AdaArgs a) {
+  extern __shared__ __attribute__((aligned(16))) bf16_t sact[];  // [16][K + 8]
+  const int wg = blockIdx.x;
+  int ei = 0;
+  while (ei + 1 < a.ne && wg >= a.e[ei + 1].wg_begin) ++ei;
+  const AdaEntry& E = a.e[ei];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int K = a.D, SST = K + 8, N = E.N, cpr = K >> 3;
+  const int nbase = (wg - E.wg_begin) * 128 + wave * 32;
+  const bf16_t* __restrict__ W = (const bf16_t*)E.W;
+  const bf16_t* __restrict__ bias = (const bf16_t*)E.bias;
+  const bf16_t* __restrict__ act = (const bf16_t*)a.act;
+  const int r16 = lane & 15, kq = lane >> 4;
+  const bf16_t* w0 = W + (long)min(nbase + r16, N - 1) * K + 8 * kq;
+  const bf16_t* w1 = W + (long)min(nbase + 16 + r16, N - 1) * K + 8 * kq;
+  const bf16_t* sp = sact + r16 * SST + 8 * kq;
+
+  for (int b0 = 0; b0 < a.B; b0 += 16) {
+    __syncthreads();
+    for (int i = tid; i < 16 * cpr; i += 256) {  // 16-byte chunks of 16 rows
+      const int r = i / cpr, c = i - r * cpr;
+      *(u32x4*)(sact + r * SST + 8 * c) = *(const u32x4*)(act + (long)(b0 + r) * K + 8 * c);
+    }
+    __syncthreads();
+    f32x4 acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll 4
+    for (int k0 = 0; k0 < K; k0 += 32) {
+      const bf16x8 a0 = *(const bf16x8*)(w0 + k0);
+      const bf16x8 a1 = *(const bf16x8*)(w1 + k0);
+      const bf16x8 bv = *(const bf16x8*)(sp + k0);
+      acc0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0, bv, acc0, 0, 0, 0);
+      acc1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1, bv, acc1, 0, 0, 0);
+    }
+    const int b = b0 + r16;
+    if (b < a.B) {
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+        const int n = nbase + 16 * t + 4 * kq;  // N is a multiple of 4
+        if (n >= N) continue;
+        const f32x4 v = t ? acc1 : acc0;
+        *(f32x4*)(E.out + (long)b * N + n) =
+            f32x4{v[0] + bf2f(bias[n]), v[1] + bf2f(bias[n + 1]), v[2] + bf2f(bias[n + 2]), v[3] + bf2f(bias[n + 3])};
+      }
+    }
+  }
+}
+
 hipError_t launch_adaln(const AdaArgs& a, int dtype, hipStream_t st) {
-  const size_t lds = (size_t)(a.B < 8 ? a.B : 8) * a.D * sizeof(float);
   dim3 grid(a.total_wg), block(256);
   if (dtype == 1) {
-    hipError_t e = hipFuncSetAttribute((const void*)adaln_kernel<bf16_t>,
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    const size_t lds = (size_t)16 * (a.D + 8) * sizeof(bf16_t);
+    hipError_t e = hipFuncSetAttribute((const void*)adaln_mfma_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                       (int)lds);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((adaln_kernel<bf16_t>), grid, block, lds, st, a);
+    hipLaunchKernelGGL(adaln_mfma_kernel, grid, block, lds, st, a);
   } else {
+    const size_t lds = (size_t)(a.B < 8 ? a.B : 8) * a.D * sizeof(float);
     hipError_t e = hipFuncSetAttribute((const void*)adaln_kernel<float>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
@@ -221,7 +294,11 @@ __global__ void timestep_feat_kernel(int B, const float* t, float* feat) {
 }
 
 // out[b][n] = post(sum_k W[n][k] in[b][k] + bias[n]); one wavefront per row n.
+// The row is loaded once into registers (8 consecutive weights per lane and
+// chunk, 16-byte loads) and dotted with every sample's input vector.
 // MODE 0: post = SiLU.  MODE 1: post = identity, plus class_table[y[b]][n].
+// K is a multiple of 8 and at most 8 * 64 * RD_MAXCH.
+constexpr int RD_MAXCH = 8;
 template <typename WT, int MODE>
 __global__ __launch_bounds__(256) void rowdot_kernel(int B, int N, int K, const float* in, const WT* W,
                                                      const WT* bias, const WT* table, const int32_t* y,
@@ -229,11 +306,32 @@ __global__ __launch_bounds__(256) void rowdot_kernel(int B, int N, int K, const 
   const int n = blockIdx.x * 4 + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   if (n >= N) return;
-  const WT* wr = W + (long)n * K;
+  const int nch = K >> 3;
+  float w[RD_MAXCH][8];
+#pragma unroll
+  for (int i = 0; i < RD_MAXCH; ++i) {
+    const int c = lane + 64 * i;
+    if (c < nch) W8<WT>::load(W + (long)n * K + c * 8, w[i]);
+    else
+#pragma unroll
+      for (int e = 0; e < 8; ++e) w[i][e] = 0.f;
+  }
+  const float bn = ld_as_float<WT>(bias, n);
   for (int b = 0; b < B; ++b) {
+    const float* xb = in + (long)b * K;
     float acc = 0.f;
-    for (int k = lane; k < K; k += 64) acc = fmaf(ld_as_float<WT>(wr, k), in[(long)b * K + k], acc);
-    acc = warp_sum(acc) + ld_as_float<WT>(bias, n);
+#pragma unroll
+    for (int i = 0; i < RD_MAXCH; ++i) {
+      const int c = lane + 64 * i;
+      if (c < nch) {
+        const float4 x0 = *(const float4*)(xb + c * 8), x1 = *(const float4*)(xb + c * 8 + 4);
+        acc = fmaf(w[i][0], x0.x, acc); acc = fmaf(w[i][1], x0.y, acc);
+        acc = fmaf(w[i][2], x0.z, acc); acc = fmaf(w[i][3], x0.w, acc);
+        acc = fmaf(w[i][4], x1.x, acc); acc = fmaf(w[i][5], x1.y, acc);
+        acc = fmaf(w[i][6], x1.z, acc); acc = fmaf(w[i][7], x1.w, acc);
+      }
+    }
+    acc = wave_sum(acc) + bn;
     if (lane == 0) {
       if (MODE == 0) out[(long)b * N + n] = acc / (1.0f + expf(-acc));
       else out[(long)b * N + n] = acc + ld_as_float<WT>(table, (long)y[b] * N + n);

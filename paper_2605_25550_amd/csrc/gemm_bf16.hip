@@ -281,15 +281,8 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs args) {
 }
 
 void gemm_tile_dims(int tile_cfg, int* bm, int* bn) {
-  switch (tile_cfg) {
-    case TILE_64x128: *bm = 64; *bn = 128; break;
-    case TILE_128x64: *bm = 128; *bn = 64; break;
-    case TILE_64x64: *bm = 64; *bn = 64; break;
-    case TILE_256x128: *bm = 256; *bn = 128; break;
-    case TILE_128x256: *bm = 128; *bn = 256; break;
-    case TILE_256x256: *bm = 256; *bn = 256; break;
-    default: *bm = 128; *bn = 128; break;
-  }
+  *bm = tile_cfg == TILE_64x128 ? 64 : 128;
+  *bn = 128;
 }
 
 template <int BM, int BN, int STAGES>
@@ -305,19 +298,12 @@ static hipError_t launch_tile(const GemmArgs& a, int epi, hipStream_t st) {
   return hipGetLastError();
 }
 
-// Stage counts: a slice is (BM + BN) x 128 bytes; the ring sizes below keep
-// two workgroups per CU up to 128x128 (measured faster than a deeper ring
-// with one workgroup) and fit 160 KB for the large tiles.
+// Ring depth: a slice is (BM + BN) x 128 bytes, so both configurations fit
+// two workgroups per CU (72 KB and 64 KB); measured faster than deeper rings
+// with one workgroup per CU.
 hipError_t launch_gemm_bf16(const GemmArgs& a, int epi, int tile_cfg, hipStream_t st) {
-  switch (tile_cfg) {
-    case TILE_64x128: return launch_tile<64, 128, 3>(a, epi, st);
-    case TILE_128x64: return launch_tile<128, 64, 3>(a, epi, st);
-    case TILE_64x64: return launch_tile<64, 64, 4>(a, epi, st);
-    case TILE_256x128: return launch_tile<256, 128, 3>(a, epi, st);
-    case TILE_128x256: return launch_tile<128, 256, 3>(a, epi, st);
-    case TILE_256x256: return launch_tile<256, 256, 2>(a, epi, st);
-    default: return launch_tile<128, 128, 2>(a, epi, st);
-  }
+  if (tile_cfg == TILE_64x128) return launch_tile<64, 128, 3>(a, epi, st);
+  return launch_tile<128, 128, 2>(a, epi, st);
 }
 
 }  // namespace ditmi

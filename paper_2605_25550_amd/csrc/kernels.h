@@ -81,6 +81,7 @@ struct AdaArgs {
   AdaEntry e[ADA_MAX_ENTRIES];
   int ne, total_wg;
   const float* cond;  // [B, D]
+  const void* act;    // bf16 path: SiLU(cond) as bf16 [round16(B), D], zero rows past B
   int B, D;
 };
 
@@ -100,6 +101,8 @@ hipError_t launch_attn_bf16(const AttnArgs& a, int head_dim, hipStream_t st);
 hipError_t launch_attn_f32(const AttnArgs& a, int head_dim, hipStream_t st);
 hipError_t launch_ln_mod(const LnArgs& a, int dtype, hipStream_t st);
 hipError_t launch_adaln(const AdaArgs& a, int dtype, hipStream_t st);
+// act[r][k] = bf16(SiLU(cond[r][k])) for r < B, 0 for B <= r < round16(B)
+hipError_t launch_silu_bf16(int B, int D, const float* cond, void* act, hipStream_t st);
 hipError_t launch_cond_embed(int B, int D, const float* t, const int32_t* y, const void* w1, const void* b1,
                              const void* w2, const void* b2, const void* table, float* feat, float* h1,
                              float* cond, int dtype, hipStream_t st);
@@ -109,10 +112,7 @@ hipError_t launch_pos_embed_2d(int gh, int gw, int D, float* pos, hipStream_t st
 hipError_t launch_prefetch(const PrefetchArgs& a, hipStream_t st);
 
 // Tile configurations of the bf16 GEMM (BM x BN).
-enum {
-  TILE_128x128 = 0, TILE_64x128 = 1, TILE_128x64 = 2, TILE_64x64 = 3,
-  TILE_256x128 = 4, TILE_128x256 = 5, TILE_256x256 = 6, TILE_COUNT = 7
-};
+enum { TILE_128x128 = 0, TILE_64x128 = 1, TILE_COUNT = 2 };
 void gemm_tile_dims(int tile_cfg, int* bm, int* bn);
 
 }  // namespace ditmi

@@ -145,6 +145,7 @@ def test_cond_pos_and_timing_validation(dm):
     z = [FAKE] * 8
     assert lib.dit_cond_embed(ctypes.byref(s), *z, FAKE, 4, None) == -3
     assert lib.dit_cond_embed(ctypes.byref(s), None, *z[1:], FAKE, 1 << 30, None) == -1
+    assert lib.dit_cond_embed(ctypes.byref(s), FAKE, FAKE, FAKE + 8, *z[3:], FAKE, 1 << 30, None) == -1  # w_t1 misaligned
     assert lib.dit_pos_embed_2d(0, 4, 8, FAKE, None) == -1
     assert lib.dit_pos_embed_2d(4, 4, 6, FAKE, None) == -1
     assert lib.dit_pos_embed_2d(4, 4, 8, None, None) == -1
