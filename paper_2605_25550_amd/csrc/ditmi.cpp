@@ -159,16 +159,17 @@ struct Gemm {
   double flops = 0, bytes = 0;
 };
 
-// bf16 tile choice (measured on MI355X, 256 CUs, two workgroups per CU):
-// 128x128 tiles are the most efficient per CU, but a launch is charged for
-// every started round of 512 tiles, so tile counts that would spill a little
-// into a second round (256..511 is one round; 512..767 is not) and counts that
-// leave most CUs idle (< 256) use 64x128 tiles instead.
+// bf16 tile choice (measured on MI355X, 256 CUs): 128x128 tiles (two
+// workgroups per CU) are the most efficient per CU, but a launch pays for
+// every started round of 512 resident tiles.  So: 128x128 for 256..511 and
+// >= 768 tiles of 128x128; between 512 and 767 (which would spill into a
+// second round) 64x128 tiles with a 2-slot ring, three per CU; below 256
+// (most CUs idle) 64x128 tiles with a 3-slot ring.
 int choose_tile(const GemmProb* p, int np) {
   long t128 = 0;
   for (int i = 0; i < np; ++i) t128 += (long)((p[i].M + 127) / 128) * ((p[i].N + 127) / 128);
-  const bool big = (t128 >= 256 && t128 < 512) || t128 >= 768;
-  return big ? TILE_128x128 : TILE_64x128;
+  if ((t128 >= 256 && t128 < 512) || t128 >= 768) return TILE_128x128;
+  return t128 >= 512 ? TILE_64x128_S2 : TILE_64x128;
 }
 
 hipError_t run_gemm(Gemm& G, int dtype, hipStream_t st) {

@@ -448,9 +448,13 @@ __global__ __launch_bounds__(256) void prefetch_kernel(PrefetchArgs a) {
   asm volatile("" : : "v"(acc));  // keep the loads
 }
 
+// 64 workgroups x 256 lanes x 8 lines in flight: the read finishes early in
+// the block (a 16-workgroup grid, streaming for longer, was measured to slow
+// the overlapped GEMMs far more).
+constexpr int PREFETCH_WGS = 64;
 hipError_t launch_prefetch(const PrefetchArgs& a, hipStream_t st) {
   if (a.n <= 0) return hipSuccess;
-  hipLaunchKernelGGL(prefetch_kernel, dim3(64), dim3(256), 0, st, a);
+  hipLaunchKernelGGL(prefetch_kernel, dim3(PREFETCH_WGS), dim3(256), 0, st, a);
   return hipGetLastError();
 }
 

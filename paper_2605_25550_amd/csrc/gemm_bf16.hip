@@ -281,7 +281,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs args) {
 }
 
 void gemm_tile_dims(int tile_cfg, int* bm, int* bn) {
-  *bm = tile_cfg == TILE_64x128 ? 64 : 128;
+  *bm = tile_cfg == TILE_128x128 ? 128 : 64;
   *bn = 128;
 }
 
@@ -298,11 +298,13 @@ static hipError_t launch_tile(const GemmArgs& a, int epi, hipStream_t st) {
   return hipGetLastError();
 }
 
-// Ring depth: a slice is (BM + BN) x 128 bytes, so both configurations fit
-// two workgroups per CU (72 KB and 64 KB); measured faster than deeper rings
-// with one workgroup per CU.
+// Ring depth: a slice is (BM + BN) x 128 bytes, so 128x128 with 2 slots and
+// 64x128 with 3 fit two workgroups per CU (64 KB, 72 KB), and 64x128 with 2
+// slots fits three (48 KB); measured faster than deeper rings with one
+// workgroup per CU.
 hipError_t launch_gemm_bf16(const GemmArgs& a, int epi, int tile_cfg, hipStream_t st) {
   if (tile_cfg == TILE_64x128) return launch_tile<64, 128, 3>(a, epi, st);
+  if (tile_cfg == TILE_64x128_S2) return launch_tile<64, 128, 2>(a, epi, st);
   return launch_tile<128, 128, 2>(a, epi, st);
 }
 
