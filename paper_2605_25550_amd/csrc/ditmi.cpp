@@ -164,19 +164,28 @@ struct Gemm {
 // every started round of 512 resident tiles.  So: 128x128 for 256..511 and
 // >= 768 tiles of 128x128; between 512 and 767 (which would spill into a
 // second round) 64x128 tiles with a 2-slot ring, three per CU; below 256
-// (most CUs idle) 64x128 tiles with a 3-slot ring.
-int choose_tile(const GemmProb* p, int np) {
-  long t128 = 0;
-  for (int i = 0; i < np; ++i) t128 += (long)((p[i].M + 127) / 128) * ((p[i].N + 127) / 128);
+// (most CUs idle) 64x144 tiles when N is a multiple of 144 and they fill the
+// CUs in one balanced round (DiT-XL/2 at 256 tokens x 8: out and fc2 become
+// exactly 256 tiles), else 64x128 tiles with a 3-slot ring.
+int choose_tile(const GemmProb* p, int np, int epi) {
+  long t128 = 0, t144 = 0;
+  bool n144 = true;
+  for (int i = 0; i < np; ++i) {
+    t128 += (long)((p[i].M + 127) / 128) * ((p[i].N + 127) / 128);
+    t144 += (long)((p[i].M + 63) / 64) * (p[i].N / 144);
+    n144 = n144 && p[i].N % 144 == 0 && (epi != EPI_QKV || (2 * p[i].hidden) % 144 == 0);
+  }
   if ((t128 >= 256 && t128 < 512) || t128 >= 768) return TILE_128x128;
-  return t128 >= 512 ? TILE_64x128_S2 : TILE_64x128;
+  if (t128 >= 512) return TILE_64x128_S2;
+  if (n144 && t144 > 192 && t144 <= 256) return TILE_64x144;
+  return TILE_64x128;
 }
 
 hipError_t run_gemm(Gemm& G, int dtype, hipStream_t st) {
   GemmArgs& a = G.a;
   int bm = 64, bn = 64, tcfg = 0;
   if (dtype == DIT_BF16) {
-    tcfg = choose_tile(a.p, a.nprob);
+    tcfg = choose_tile(a.p, a.nprob, G.epi);
     gemm_tile_dims(tcfg, &bm, &bn);
   }
   int tiles = 0;

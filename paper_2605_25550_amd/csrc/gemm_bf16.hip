@@ -62,6 +62,83 @@ __device__ __forceinline__ void dma_16s(const void* sbase, unsigned voff, unsign
                : "memory", "m0");
 }
 
+// Epilogue of one LDS-staged slab of fp32 accumulators: 32 rows starting at
+// global row mb, WTN columns starting at global column nw0, row stride CST.
+// Each lane takes four consecutive columns of one row (or, for the v part of
+// the QKV projection, one column and four consecutive rows) and applies the
+// fused epilogue with 8- or 16-byte global accesses.
+template <int EPI, int WTN, int CST>
+__device__ __forceinline__ void epilogue_slab(const GemmProb& P, const float* Cw, int mb, int nw0, bool vcols,
+                                              int lane) {
+  const bf16_t* __restrict__ bias = (const bf16_t*)P.bias;
+  const int rpb = P.rows_per_batch, M = P.M, N = P.N;
+  constexpr int PER_LANE = 32 * WTN / 4 / 64;  // 4-element groups per lane per slab
+  static_assert(32 * WTN % 256 == 0, "slab must split evenly over 64 lanes");
+  if (vcols) {
+    // v^T[b][h][d][j]: lane takes one column and four consecutive rows.
+    const int D = P.hidden, dh = P.head_dim;
+#pragma unroll
+    for (int it = 0; it < PER_LANE; ++it) {
+      const int c = lane + 64 * it;
+      const int col = c >> 3, r4 = (c & 7) * 4;
+      const int n = nw0 + col, m = mb + r4;
+      if (n >= N || m >= M) continue;
+      const int rem = n - 2 * D, h = rem / dh, d = rem - h * dh;
+      const float bv = bf2f(bias[n]);
+      const int b = m / rpb, jp = m - b * rpb + P.seq_off;
+      const float v0 = Cw[(r4 + 0) * CST + col] + bv, v1 = Cw[(r4 + 1) * CST + col] + bv;
+      const float v2 = Cw[(r4 + 2) * CST + col] + bv, v3 = Cw[(r4 + 3) * CST + col] + bv;
+      if (m + 3 < M && (m + 3) / rpb == b && (jp & 3) == 0) {
+        bf16_t* vt = (bf16_t*)P.v + (((long)b * P.heads + h) * dh + d) * P.Tj_pad + jp;
+        *(u32x2*)vt = u32x2{pack_bf16x2(v0, v1), pack_bf16x2(v2, v3)};
+      } else {
+        const float vv[4] = {v0, v1, v2, v3};
+        for (int e = 0; e < 4 && m + e < M; ++e) {
+          const int be = (m + e) / rpb, je = (m + e) - be * rpb + P.seq_off;
+          ((bf16_t*)P.v)[(((long)be * P.heads + h) * dh + d) * P.Tj_pad + je] = f2bf(vv[e]);
+        }
+      }
+    }
+    return;
+  }
+  constexpr int CPR = WTN / 4;  // 4-column groups per slab row
+#pragma unroll
+  for (int it = 0; it < PER_LANE; ++it) {
+    const int c = lane + 64 * it;
+    const int row = c / CPR, c4 = (c % CPR) * 4;
+    const int m = mb + row, n = nw0 + c4;
+    if (m >= M || n >= N) continue;  // N is a multiple of 4
+    const f32x4 y = *(const f32x4*)&Cw[row * CST + c4];
+    const u32x2 bw2 = *(const u32x2*)(bias + n);
+    const float y0 = y[0] + __uint_as_float(bw2[0] << 16), y1 = y[1] + __uint_as_float(bw2[0] & 0xFFFF0000u);
+    const float y2 = y[2] + __uint_as_float(bw2[1] << 16), y3 = y[3] + __uint_as_float(bw2[1] & 0xFFFF0000u);
+    if (EPI == EPI_RESID || EPI == EPI_RESID2) {
+      const int b = m / rpb;
+      f32x4* xr = (f32x4*)(P.resid + (long)m * N + n);
+      const f32x4 gt = *(const f32x4*)(P.gate + (long)b * P.gate_stride + n);
+      f32x4 xv = *xr;
+      xv[0] += gt[0] * y0;
+      xv[1] += gt[1] * y1;
+      xv[2] += gt[2] * y2;
+      xv[3] += gt[3] * y3;
+      *xr = xv;
+    } else if (EPI == EPI_GELU) {
+      *(u32x2*)((bf16_t*)P.out + (long)m * N + n) =
+          u32x2{pack_bf16x2(gelu_tanh(y0), gelu_tanh(y1)), pack_bf16x2(gelu_tanh(y2), gelu_tanh(y3))};
+    } else if (EPI == EPI_STORE) {
+      *(f32x4*)((float*)P.out + (long)m * N + n) = f32x4{y0, y1, y2, y3};
+    } else {  // EPI_QKV, q and k columns: 4 consecutive d of one head
+      const int D = P.hidden, dh = P.head_dim;
+      const int s = n / D, rem = n - s * D, h = rem / dh, d = rem - h * dh;
+      const int b = m / rpb, jp = m - b * rpb + P.seq_off;
+      bf16_t* dst = (bf16_t*)(s == 0 ? P.q : P.k) + (((long)b * P.heads + h) * P.Tj + jp) * P.qk_stride + d;
+      *(u32x2*)dst = u32x2{pack_bf16x2(y0, y1), pack_bf16x2(y2, y3)};
+      if (d + 4 == dh && P.qk_stride > dh)  // zero the row's padding (head_dim 72 -> 80)
+        for (int z = 4; z < P.qk_stride - dh + 4; z += 4) *(u32x2*)(dst + z) = u32x2{0u, 0u};
+    }
+  }
+}
+
 template <int BM, int BN, int STAGES, int EPI>
 __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs args) {
   using C = GemmCfg<BM, BN, STAGES>;
@@ -197,12 +274,9 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs args) {
   // Per 32-row slab i: each wave writes its 32 x (BN/2) accumulators to its
   // own LDS region (column r32 + 32j, rows 8*jj + 4*g + ii), then reads them
   // back four columns (or, for v^T, four rows) per lane.
-  const bf16_t* __restrict__ bias = (const bf16_t*)P.bias;
-  const int rpb = P.rows_per_batch;
   float* const Cw = reinterpret_cast<float*>(smem) + wave * 32 * C::CST;
   const int nw0 = n0 + wn * C::WTN;
-  const bool vcols = EPI == EPI_QKV && n0 >= 2 * P.hidden;  // tiles never straddle k|v (2D % 128 == 0)
-  constexpr int PER_LANE = 32 * C::WTN / 4 / 64;               // 4-element groups per lane per slab
+  const bool vcols = EPI == EPI_QKV && n0 >= 2 * P.hidden;  // tiles never straddle k|v (2D % BN == 0)
 #pragma unroll
   for (int i = 0; i < C::TM; ++i) {
     __syncthreads();
@@ -213,76 +287,183 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs args) {
 #pragma unroll
         for (int ii = 0; ii < 4; ++ii) Cw[(jj * 8 + g * 4 + ii) * C::CST + j * 32 + r32] = acc[i][j][jj * 4 + ii];
     __syncthreads();
-    const int mb = m0 + wm * C::WTM + i * 32;
-    if (vcols) {
-      // v^T[b][h][d][j]: lane takes one column and four consecutive rows.
-      const int D = P.hidden, dh = P.head_dim;
+    epilogue_slab<EPI, C::WTN, C::CST>(P, Cw, m0 + wm * C::WTM + i * 32, nw0, vcols, lane);
+  }
+}
+
+// ---------------------------------------------------------------- 64 x 144 tiles
+// For N a multiple of 144 (the DiT-XL widths 1152 = 8*144, 3456 = 24*144,
+// 4608 = 32*144), 64 x 144 tiles make the tile count a multiple of 256 at the
+// DiT-XL/2 token counts (2048 or 4096 rows), so every CU gets the same work;
+// 64 x 128 or 128 x 128 tiles there leave part of the last round idle.
+// Six waves (2 x 3), each owning 32 x 48 as 2 x 3 accumulators of
+// v_mfma_f32_16x16x32_bf16 (lane: row lane%16 of A and of W, k offset
+// 8*(lane/16) + 32*step; D: column lane%16, rows 4*(lane/16) + i).  Same
+// slice format, swizzle, DMA ring and refill rule as the kernel above; the
+// slice's 26 DMA instructions are spread 5 per wave, and the 4 spare ones
+// re-read a valid row into a dummy LDS line.  The ring (3 x 26 KB) lets two
+// workgroups share a CU.
+struct Gemm144 {
+  static constexpr int BM = 64, BN = 144, BK = 64, STAGES = 3, NW = 6;
+  static constexpr int ROWS = BM + BN;                // 208
+  static constexpr int SLICE = ROWS * 128;            // bytes per slice buffer
+  static constexpr int NDMA = ROWS / 8;               // 26 DMA instructions per slice
+  static constexpr int IPW = (NDMA + NW - 1) / NW;    // 5 per wave
+  static constexpr int TM = 2, TN = 3, WTM = 32, WTN = 48;
+  static constexpr int CST = WTN + 4;                 // fp32 row stride of an epilogue slab
+  static constexpr int SPARE = STAGES * SLICE;        // dummy target of the spare DMAs
+  static constexpr int LDS_MAIN = SPARE + 1024;
+  static constexpr int LDS_EPI = NW * 32 * CST * 4;
+  static constexpr int LDS = LDS_MAIN > LDS_EPI ? LDS_MAIN : LDS_EPI;
+  static_assert((STAGES - 1) * IPW < 64, "vmcnt range");
+  static_assert(2 * LDS <= 160 * 1024, "two workgroups per CU");
+};
+
+template <int EPI>
+__global__ __launch_bounds__(384) void gemm_bf16_144_kernel(GemmArgs args) {
+  using C = Gemm144;
+  __shared__ __attribute__((aligned(1024))) unsigned char smem[C::LDS];
+
+  const int tile = xcd_remap(blockIdx.x, args.total_tiles);
+  const bool second = args.nprob > 1 && tile >= args.p[1].tile_begin;
+  const GemmProb P = second ? args.p[1] : args.p[0];
+  const int local = tile - P.tile_begin;
+  const int GM = 8;
+  const int group_size = GM * P.tiles_n;
+  const int group = local / group_size;
+  const int first_m = group * GM;
+  const int gm = min(P.tiles_m - first_m, GM);
+  const int in_group = local - group * group_size;
+  const int m0 = (first_m + in_group % gm) * C::BM;
+  const int n0 = (in_group / gm) * C::BN;
+
+  const bf16_t* __restrict__ A = (const bf16_t*)P.A;
+  const bf16_t* __restrict__ W = (const bf16_t*)P.W;
+  const int M = P.M, N = P.N, K = P.K;
+  const int KT = K / C::BK;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave / 3, wn = wave - 3 * wm;
+  const int r16 = lane & 15, g4 = lane >> 4;
+  const unsigned lds0 = __builtin_amdgcn_readfirstlane(lds_address(smem));
+
+  // DMA instruction t of this wave fills slice rows 8q .. 8q+7, q = wave + 6t
+  // (A rows for q < 8, W rows for q < 26, spare above); lane -> row 8q +
+  // lane/8 at stored position lane%8, i.e. chunk (lane%8) ^ (lane/8) ^ (q&1).
+  const int cfetch = (lane & 7) ^ (lane >> 3) ^ (wave & 1);
+  unsigned voff[C::IPW];
 #pragma unroll
-      for (int it = 0; it < PER_LANE; ++it) {
-        const int c = lane + 64 * it;
-        const int col = c >> 3, r4 = (c & 7) * 4;
-        const int n = nw0 + col, m = mb + r4;
-        if (n >= N || m >= M) continue;
-        const int rem = n - 2 * D, h = rem / dh, d = rem - h * dh;
-        const float bv = bf2f(bias[n]);
-        const int b = m / rpb, jp = m - b * rpb + P.seq_off;
-        const float v0 = Cw[(r4 + 0) * C::CST + col] + bv, v1 = Cw[(r4 + 1) * C::CST + col] + bv;
-        const float v2 = Cw[(r4 + 2) * C::CST + col] + bv, v3 = Cw[(r4 + 3) * C::CST + col] + bv;
-        if (m + 3 < M && (m + 3) / rpb == b && (jp & 3) == 0) {
-          bf16_t* vt = (bf16_t*)P.v + (((long)b * P.heads + h) * dh + d) * P.Tj_pad + jp;
-          *(u32x2*)vt = u32x2{pack_bf16x2(v0, v1), pack_bf16x2(v2, v3)};
-        } else {
-          const float vv[4] = {v0, v1, v2, v3};
-          for (int e = 0; e < 4 && m + e < M; ++e) {
-            const int be = (m + e) / rpb, je = (m + e) - be * rpb + P.seq_off;
-            ((bf16_t*)P.v)[(((long)be * P.heads + h) * dh + d) * P.Tj_pad + je] = f2bf(vv[e]);
-          }
-        }
-      }
-      continue;
+  for (int t = 0; t < C::IPW; ++t) {
+    const int q = wave + C::NW * t;
+    const int row = 8 * q + (lane >> 3);
+    const int grow = q < C::BM / 8 ? min(m0 + row, M - 1) : q < C::NDMA ? min(n0 + row - C::BM, N - 1) : 0;
+    voff[t] = (unsigned)grow * (unsigned)K * 2u + (unsigned)cfetch * 16u;
+  }
+  auto issue = [&](int slice, int slot) {
+    const long kb = (long)slice * C::BK;
+    const bf16_t* sa = A + kb;
+    const bf16_t* sw = W + kb;
+    const unsigned base = lds0 + (unsigned)(slot * C::SLICE);
+#pragma unroll
+    for (int t = 0; t < C::IPW; ++t) {
+      const int q = wave + C::NW * t;  // wave-uniform
+      const unsigned dst = q < C::NDMA ? base + (unsigned)(q * 1024) : lds0 + (unsigned)C::SPARE;
+      dma_16s(q < C::BM / 8 || q >= C::NDMA ? sa : sw, voff[t], dst);
     }
-    constexpr int CPR = C::WTN / 4;  // 4-column groups per slab row
+  };
+
+  // fragment offsets per 32-wide k-step s (two per slice)
+  int a_off[2][C::TM], b_off[2][C::TN];
 #pragma unroll
-    for (int it = 0; it < PER_LANE; ++it) {
-      const int c = lane + 64 * it;
-      const int row = c / CPR, c4 = (c % CPR) * 4;
-      const int m = mb + row, n = nw0 + c4;
-      if (m >= M || n >= N) continue;  // N is a multiple of 4
-      const f32x4 y = *(const f32x4*)&Cw[row * C::CST + c4];
-      const u32x2 bw2 = *(const u32x2*)(bias + n);
-      const float y0 = y[0] + __uint_as_float(bw2[0] << 16), y1 = y[1] + __uint_as_float(bw2[0] & 0xFFFF0000u);
-      const float y2 = y[2] + __uint_as_float(bw2[1] << 16), y3 = y[3] + __uint_as_float(bw2[1] & 0xFFFF0000u);
-      if (EPI == EPI_RESID || EPI == EPI_RESID2) {
-        const int b = m / rpb;
-        f32x4* xr = (f32x4*)(P.resid + (long)m * N + n);
-        const f32x4 gt = *(const f32x4*)(P.gate + (long)b * P.gate_stride + n);
-        f32x4 xv = *xr;
-        xv[0] += gt[0] * y0;
-        xv[1] += gt[1] * y1;
-        xv[2] += gt[2] * y2;
-        xv[3] += gt[3] * y3;
-        *xr = xv;
-      } else if (EPI == EPI_GELU) {
-        *(u32x2*)((bf16_t*)P.out + (long)m * N + n) =
-            u32x2{pack_bf16x2(gelu_tanh(y0), gelu_tanh(y1)), pack_bf16x2(gelu_tanh(y2), gelu_tanh(y3))};
-      } else if (EPI == EPI_STORE) {
-        *(f32x4*)((float*)P.out + (long)m * N + n) = f32x4{y0, y1, y2, y3};
-      } else {  // EPI_QKV, q and k columns: 4 consecutive d of one head
-        const int D = P.hidden, dh = P.head_dim;
-        const int s = n / D, rem = n - s * D, h = rem / dh, d = rem - h * dh;
-        const int b = m / rpb, jp = m - b * rpb + P.seq_off;
-        bf16_t* dst = (bf16_t*)(s == 0 ? P.q : P.k) + (((long)b * P.heads + h) * P.Tj + jp) * P.qk_stride + d;
-        *(u32x2*)dst = u32x2{pack_bf16x2(y0, y1), pack_bf16x2(y2, y3)};
-        if (d + 4 == dh && P.qk_stride > dh)  // zero the row's padding (head_dim 72 -> 80)
-          for (int z = 4; z < P.qk_stride - dh + 4; z += 4) *(u32x2*)(dst + z) = u32x2{0u, 0u};
-      }
+  for (int s = 0; s < 2; ++s) {
+    const int c = 4 * s + g4;
+#pragma unroll
+    for (int i = 0; i < C::TM; ++i) {
+      const int R = wm * C::WTM + i * 16 + r16;
+      a_off[s][i] = R * 128 + (chunk_pos(R, c) << 4);
+    }
+#pragma unroll
+    for (int j = 0; j < C::TN; ++j) {
+      const int R = C::BM + wn * C::WTN + j * 16 + r16;
+      b_off[s][j] = R * 128 + (chunk_pos(R, c) << 4);
     }
   }
+
+  f32x4 acc[C::TM][C::TN];
+#pragma unroll
+  for (int i = 0; i < C::TM; ++i)
+#pragma unroll
+    for (int j = 0; j < C::TN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  bf16x8 xa[C::TM], xb[C::TN], ya[C::TM], yb[C::TN];
+#define G144_READ(FA, FB, slot, s)                                                            \
+  do {                                                                                       \
+    const unsigned char* b_ = smem + (slot) * C::SLICE;                                      \
+    _Pragma("unroll") for (int i = 0; i < C::TM; ++i) FA[i] = *(const bf16x8*)(b_ + a_off[s][i]); \
+    _Pragma("unroll") for (int j = 0; j < C::TN; ++j) FB[j] = *(const bf16x8*)(b_ + b_off[s][j]); \
+  } while (0)
+#define G144_MFMA(FA, FB)                                                                     \
+  _Pragma("unroll") for (int i = 0; i < C::TM; ++i) _Pragma("unroll") for (int j = 0; j < C::TN; ++j) \
+    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(FA[i], FB[j], acc[i][j], 0, 0, 0);
+#define SCHED_FENCE() __builtin_amdgcn_sched_barrier(0)
+
+#pragma unroll
+  for (int s = 0; s < C::STAGES; ++s)
+    if (s < KT) issue(s, s);
+  if (KT >= C::STAGES) wait_vmcnt<(C::STAGES - 1) * C::IPW>();
+  else wait_vmcnt<0>();
+  __syncthreads();
+  G144_READ(xa, xb, 0, 0);
+  int slot = 0;
+  for (int kt = 0; kt < KT; ++kt) {
+    const int next = slot + 1 == C::STAGES ? 0 : slot + 1;
+    G144_READ(ya, yb, slot, 1);
+    SCHED_FENCE();
+    G144_MFMA(xa, xb);
+    SCHED_FENCE();
+    if (kt + C::STAGES - 1 < KT) wait_vmcnt<(C::STAGES - 2) * C::IPW>();  // own DMA of slice kt+1 landed
+    else wait_vmcnt<0>();
+    __syncthreads();
+    if (kt + C::STAGES < KT) issue(kt + C::STAGES, slot);
+    G144_READ(xa, xb, next, 0);  // past the last slice this reads stale data, unused
+    SCHED_FENCE();
+    G144_MFMA(ya, yb);
+    SCHED_FENCE();
+    slot = next;
+  }
+#undef G144_READ
+#undef G144_MFMA
+#undef SCHED_FENCE
+
+  // epilogue: each wave stages its 32 x 48 accumulators in its own LDS region
+  float* const Cw = reinterpret_cast<float*>(smem) + wave * 32 * C::CST;
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < C::TM; ++i)
+#pragma unroll
+    for (int j = 0; j < C::TN; ++j)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) Cw[(i * 16 + 4 * g4 + e) * C::CST + j * 16 + r16] = acc[i][j][e];
+  __syncthreads();
+  const bool vcols = EPI == EPI_QKV && n0 >= 2 * P.hidden;  // the host only picks 144 when 2D % 144 == 0
+  epilogue_slab<EPI, C::WTN, C::CST>(P, Cw, m0 + wm * C::WTM, n0 + wn * C::WTN, vcols, lane);
 }
 
 void gemm_tile_dims(int tile_cfg, int* bm, int* bn) {
   *bm = tile_cfg == TILE_128x128 ? 128 : 64;
-  *bn = 128;
+  *bn = tile_cfg == TILE_64x144 ? 144 : 128;
+}
+
+static hipError_t launch_144(const GemmArgs& a, int epi, hipStream_t st) {
+  dim3 grid(a.total_tiles), block(Gemm144::NW * 64);
+  switch (epi) {
+    case EPI_QKV: hipLaunchKernelGGL((gemm_bf16_144_kernel<EPI_QKV>), grid, block, 0, st, a); break;
+    case EPI_GELU: hipLaunchKernelGGL((gemm_bf16_144_kernel<EPI_GELU>), grid, block, 0, st, a); break;
+    case EPI_RESID: hipLaunchKernelGGL((gemm_bf16_144_kernel<EPI_RESID>), grid, block, 0, st, a); break;
+    case EPI_RESID2: hipLaunchKernelGGL((gemm_bf16_144_kernel<EPI_RESID2>), grid, block, 0, st, a); break;
+    default: hipLaunchKernelGGL((gemm_bf16_144_kernel<EPI_STORE>), grid, block, 0, st, a); break;
+  }
+  return hipGetLastError();
 }
 
 template <int BM, int BN, int STAGES>
@@ -305,6 +486,7 @@ static hipError_t launch_tile(const GemmArgs& a, int epi, hipStream_t st) {
 hipError_t launch_gemm_bf16(const GemmArgs& a, int epi, int tile_cfg, hipStream_t st) {
   if (tile_cfg == TILE_64x128) return launch_tile<64, 128, 3>(a, epi, st);
   if (tile_cfg == TILE_64x128_S2) return launch_tile<64, 128, 2>(a, epi, st);
+  if (tile_cfg == TILE_64x144) return launch_144(a, epi, st);
   return launch_tile<128, 128, 2>(a, epi, st);
 }
 

@@ -112,7 +112,7 @@ hipError_t launch_pos_embed_2d(int gh, int gw, int D, float* pos, hipStream_t st
 hipError_t launch_prefetch(const PrefetchArgs& a, hipStream_t st);
 
 // Tile configurations of the bf16 GEMM (BM x BN, LDS ring depth).
-enum { TILE_128x128 = 0, TILE_64x128 = 1, TILE_64x128_S2 = 2, TILE_COUNT = 3 };
+enum { TILE_128x128 = 0, TILE_64x128 = 1, TILE_64x128_S2 = 2, TILE_64x144 = 3, TILE_COUNT = 4 };
 void gemm_tile_dims(int tile_cfg, int* bm, int* bn);
 
 }  // namespace ditmi

@@ -167,6 +167,12 @@ def test_block_c1_full():
     block_case(synth.CONFIGS["c1"].with_(n_blocks=1))
 
 
+def test_block_c1_ragged_rows():
+    """B=7, T=250: 1750 rows, a ragged last row tile; the out and fc2 GEMMs
+    (N = 1152) take the 64x144 tile path at this size (224 tiles)."""
+    block_case(synth.CONFIGS["c1"].with_(batch=7, tokens=250, n_blocks=1))
+
+
 def test_block_c2_full():
     block_case(synth.CONFIGS["c2"].with_(n_blocks=1))
 
