@@ -55,6 +55,17 @@ __device__ __forceinline__ float wave_sum(float v) {
          (__int_as_float(__builtin_amdgcn_readlane(b, 32)) + __int_as_float(__builtin_amdgcn_readlane(b, 48)));
 }
 
+// n / d for 0 <= n < 2^24, d >= 1 and a quotient below 2^22, given
+// inv = 1.0f / d (correctly rounded): the float estimate is within one of the
+// quotient, and the two integer corrections make it exact.  Cheaper than the
+// integer division sequence for a runtime divisor.
+__device__ __forceinline__ int div_exact(int n, int d, float inv) {
+  int q = (int)((float)n * inv);
+  q -= q * d > n ? 1 : 0;
+  q += (q + 1) * d <= n ? 1 : 0;
+  return q;
+}
+
 // Value held by lane (l ^ 32): the other half of a 64-wide wavefront.
 __device__ __forceinline__ float other_half(float v) { return __shfl_xor(v, 32, 64); }
 

@@ -72,6 +72,8 @@ __device__ __forceinline__ void epilogue_slab(const GemmProb& P, const float* Cw
                                               int lane) {
   const bf16_t* __restrict__ bias = (const bf16_t*)P.bias;
   const int rpb = P.rows_per_batch, M = P.M, N = P.N;
+  const float inv_rpb = 1.0f / (float)rpb;  // wave-uniform, for div_exact
+  const float inv_dh = 1.0f / (float)P.head_dim, inv_D = 1.0f / (float)P.hidden;
   constexpr int PER_LANE = 32 * WTN / 4 / 64;  // 4-element groups per lane per slab
   static_assert(32 * WTN % 256 == 0, "slab must split evenly over 64 lanes");
   if (vcols) {
@@ -83,18 +85,18 @@ __device__ __forceinline__ void epilogue_slab(const GemmProb& P, const float* Cw
       const int col = c >> 3, r4 = (c & 7) * 4;
       const int n = nw0 + col, m = mb + r4;
       if (n >= N || m >= M) continue;
-      const int rem = n - 2 * D, h = rem / dh, d = rem - h * dh;
+      const int rem = n - 2 * D, h = div_exact(rem, dh, inv_dh), d = rem - h * dh;
       const float bv = bf2f(bias[n]);
-      const int b = m / rpb, jp = m - b * rpb + P.seq_off;
+      const int b = div_exact(m, rpb, inv_rpb), jp = m - b * rpb + P.seq_off;
       const float v0 = Cw[(r4 + 0) * CST + col] + bv, v1 = Cw[(r4 + 1) * CST + col] + bv;
       const float v2 = Cw[(r4 + 2) * CST + col] + bv, v3 = Cw[(r4 + 3) * CST + col] + bv;
-      if (m + 3 < M && (m + 3) / rpb == b && (jp & 3) == 0) {
+      if (m + 3 < M && jp - P.seq_off + 3 < rpb && (jp & 3) == 0) {
         bf16_t* vt = (bf16_t*)P.v + (((long)b * P.heads + h) * dh + d) * P.Tj_pad + jp;
         *(u32x2*)vt = u32x2{pack_bf16x2(v0, v1), pack_bf16x2(v2, v3)};
       } else {
         const float vv[4] = {v0, v1, v2, v3};
         for (int e = 0; e < 4 && m + e < M; ++e) {
-          const int be = (m + e) / rpb, je = (m + e) - be * rpb + P.seq_off;
+          const int be = div_exact(m + e, rpb, inv_rpb), je = (m + e) - be * rpb + P.seq_off;
           ((bf16_t*)P.v)[(((long)be * P.heads + h) * dh + d) * P.Tj_pad + je] = f2bf(vv[e]);
         }
       }
@@ -113,7 +115,7 @@ __device__ __forceinline__ void epilogue_slab(const GemmProb& P, const float* Cw
     const float y0 = y[0] + __uint_as_float(bw2[0] << 16), y1 = y[1] + __uint_as_float(bw2[0] & 0xFFFF0000u);
     const float y2 = y[2] + __uint_as_float(bw2[1] << 16), y3 = y[3] + __uint_as_float(bw2[1] & 0xFFFF0000u);
     if (EPI == EPI_RESID || EPI == EPI_RESID2) {
-      const int b = m / rpb;
+      const int b = div_exact(m, rpb, inv_rpb);
       f32x4* xr = (f32x4*)(P.resid + (long)m * N + n);
       const f32x4 gt = *(const f32x4*)(P.gate + (long)b * P.gate_stride + n);
       f32x4 xv = *xr;
@@ -129,8 +131,8 @@ __device__ __forceinline__ void epilogue_slab(const GemmProb& P, const float* Cw
       *(f32x4*)((float*)P.out + (long)m * N + n) = f32x4{y0, y1, y2, y3};
     } else {  // EPI_QKV, q and k columns: 4 consecutive d of one head
       const int D = P.hidden, dh = P.head_dim;
-      const int s = n / D, rem = n - s * D, h = rem / dh, d = rem - h * dh;
-      const int b = m / rpb, jp = m - b * rpb + P.seq_off;
+      const int s = div_exact(n, D, inv_D), rem = n - s * D, h = div_exact(rem, dh, inv_dh), d = rem - h * dh;
+      const int b = div_exact(m, rpb, inv_rpb), jp = m - b * rpb + P.seq_off;
       bf16_t* dst = (bf16_t*)(s == 0 ? P.q : P.k) + (((long)b * P.heads + h) * P.Tj + jp) * P.qk_stride + d;
       *(u32x2*)dst = u32x2{pack_bf16x2(y0, y1), pack_bf16x2(y2, y3)};
       if (d + 4 == dh && P.qk_stride > dh)  // zero the row's padding (head_dim 72 -> 80)
