@@ -83,14 +83,22 @@ __device__ __forceinline__ float sum_halves(float v) {
 }
 
 // tanh-approximated GELU; tanh(z) = 1 - 2 / (exp(2z) + 1).
+// tanh-GELU: 0.5 u (1 + tanh z) with z = sqrt(2/pi) (u + 0.044715 u^3), in the
+// equivalent form u / (1 + exp(-2z)) = u * rcp(1 + exp2(u (c1 + c2 u^2))),
+// c1 = -2 log2(e) sqrt(2/pi), c2 = 0.044715 c1.  v_rcp_f32 is within 1 ulp,
+// far below the bf16 rounding of the GELU output (and the fp32 path's
+// tolerance); exp2 overflow to +inf gives the exact limit 0.
 __device__ __forceinline__ float gelu_tanh(float u) {
-  const float k0 = 0.7978845608028654f;  // sqrt(2/pi)
-  float z = k0 * (u + 0.044715f * u * u * u);
-  float t = 1.0f - 2.0f / (__expf(2.0f * z) + 1.0f);
-  return 0.5f * u * (1.0f + t);
+  const float c1 = -2.30220819814f;           // -2 * log2(e) * sqrt(2/pi)
+  const float c2 = -0.10294323958f;           // 0.044715 * c1
+  const float e = __builtin_amdgcn_exp2f(u * fmaf(c2, u * u, c1));
+  return u * __builtin_amdgcn_rcpf(1.0f + e);
 }
 
-__device__ __forceinline__ float silu(float z) { return z / (1.0f + __expf(-z)); }
+// SiLU z / (1 + exp(-z)) with the hardware reciprocal (within 1 ulp).
+__device__ __forceinline__ float silu(float z) {
+  return z * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(-1.4426950408889634f * z));
+}
 
 // Workgroup id -> logical tile id so that consecutive logical tiles land on
 // the same XCD (workgroups are dispatched round-robin over the 8 XCDs).
