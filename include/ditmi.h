@@ -35,6 +35,13 @@
  *     they propagate.  No call aborts or throws.
  *   - dit_last_error() returns the text of the calling thread's last failure.
  *   - Calls are thread-safe; concurrent calls must not share a workspace.
+ *   - dit_step_forward may enqueue advisory work on one internal stream per
+ *     (calling thread, device), created at first use with default priority:
+ *     reads of the next block's weights into the Infinity Cache.  It is
+ *     forked from and joined back into `stream` with events inside the call,
+ *     so all later work on `stream` (including freeing the weights) is
+ *     ordered after it, and the call can be captured into a HIP graph.
+ *     No allocation or memset is enqueued by any call.
  */
 #ifndef DITMI_H
 #define DITMI_H

@@ -424,3 +424,90 @@ def test_generator_inputs_all_configs():
             assert np.all((inp["t"] >= 0) & (inp["t"] < 1000)) and np.all((inp["y"] >= 0) & (inp["y"] < 1000))
         np.testing.assert_array_equal(synth.inputs(small)["x"], inp["x"])
         assert not np.array_equal(synth.inputs(small, salt=1)["x"], inp["x"])
+
+
+# ------------------------------------------------------------ multi-step sampler loop
+def _zero_network(cfg, seed=50):
+    """Step weights and blocks whose velocity is the constant b_final: every
+    block has zero gates (identity) and the final projection is zero."""
+    D = cfg.hidden
+    sw = {k: v.astype(np.float64) for k, v in synth.step_weights(cfg).items()}
+    sw["w_final"] = np.zeros_like(sw["w_final"])
+    sw["b_final"] = rand(sw["b_final"].shape, seed)
+    blocks = []
+    for l in range(cfg.n_blocks):
+        w = weights(cfg, block=l)
+        for ch in (2, 5):
+            w["w_ada"][ch * D:(ch + 1) * D] = 0.0
+            w["b_ada"][ch * D:(ch + 1) * D] = 0.0
+        blocks.append({"img": w})
+    return sw, blocks
+
+
+@pytest.mark.parametrize("sigmas", [[1.0, 0.75, 0.5, 0.25, 0.0], [1.0, 0.875, 0.5, 0.125, 0.0], [0.0, 0.5, 1.0]])
+@pytest.mark.parametrize("class_cond", [False, True])
+def test_sampler_constant_velocity_closed_form(sigmas, class_cond):
+    """Constant velocity b: the Euler loop integrates dz/dsigma = b exactly,
+    z_n = z_0 + (sigma_n - sigma_0) b (dyadic schedules: float32 differences are exact)."""
+    cfg = tiny_cfg(n_blocks=2, patch_in=6, patch_out=6, batch=2, cond="class" if class_cond else "given")
+    sw, blocks = _zero_network(cfg)
+    z0 = rand((cfg.batch, cfg.tokens, 6), 51)
+    kw = {"y": np.array([3, 7])} if class_cond else {"cond": rand((cfg.batch, cfg.hidden), 52)}
+    z = O.sample_euler(cfg, z0, sigmas, sw, blocks, **kw)
+    want = z0 + (sigmas[-1] - sigmas[0]) * sw["b_final"][None, None, :]
+    np.testing.assert_allclose(z, want, rtol=0, atol=1e-12)
+
+
+def test_sampler_zero_steps_is_identity():
+    cfg = tiny_cfg(n_blocks=1, patch_in=6, patch_out=6)
+    sw = {k: v.astype(np.float64) for k, v in synth.step_weights(cfg).items()}
+    z0 = rand((cfg.batch, cfg.tokens, 6), 53)
+    z = O.sample_euler(cfg, z0, [0.7], sw, [{"img": weights(cfg)}], cond=rand((cfg.batch, cfg.hidden), 54))
+    assert np.array_equal(z, z0)
+
+
+def test_sampler_splits_into_consecutive_runs():
+    """The loop is a sequence of independent steps: running [a, b, c] equals
+    running [a, b] and then [b, c] from its result, bitwise."""
+    cfg = tiny_cfg(n_blocks=2, patch_in=6, patch_out=6, batch=2, cond="class")
+    sw = {k: v.astype(np.float64) for k, v in synth.step_weights(cfg).items()}
+    blocks = [{"img": weights(cfg, block=l)} for l in range(2)]
+    z0 = rand((cfg.batch, cfg.tokens, 6), 55)
+    y = np.array([1, 900])
+    whole = O.sample_euler(cfg, z0, [1.0, 0.6, 0.3, 0.0], sw, blocks, y=y)
+    part = O.sample_euler(cfg, z0, [1.0, 0.6], sw, blocks, y=y)
+    rest = O.sample_euler(cfg, part, [0.6, 0.3, 0.0], sw, blocks, y=y)
+    assert np.array_equal(whole, rest)
+
+
+def test_sampler_step_uses_left_endpoint_conditioning():
+    """One step: z1 = z0 + (s1 - s0) v(z0, c(t0)), t0 = s0 * 1000 in float32;
+    the conditioning at the other endpoint gives a different result."""
+    cfg = tiny_cfg(n_blocks=2, patch_in=6, patch_out=6, batch=2, cond="class")
+    sw = {k: v.astype(np.float64) for k, v in synth.step_weights(cfg).items()}
+    blocks = [{"img": weights(cfg, block=l)} for l in range(2)]
+    z0 = rand((cfg.batch, cfg.tokens, 6), 56)
+    y = np.array([4, 5])
+    s0, s1 = 0.8, 0.3
+    z1 = O.sample_euler(cfg, z0, [s0, s1], sw, blocks, y=y)
+    cw = [sw[k] for k in ("w_t1", "b_t1", "w_t2", "b_t2", "class_table")]
+    t0 = np.full(2, np.float32(np.float32(s0) * np.float32(1000.0)), dtype=np.float64)
+    v0, _ = O.dit_step(cfg, z0, O.class_conditioning(t0, y, *cw), sw, blocks)
+    np.testing.assert_allclose(z1, z0 + float(np.float32(s1) - np.float32(s0)) * v0, rtol=0, atol=1e-12)
+    v1, _ = O.dit_step(cfg, z0, O.class_conditioning(np.full(2, 300.0), y, *cw), sw, blocks)
+    assert np.max(np.abs(v1 - v0)) > 1e-6
+
+
+def test_sampler_joint_restarts_text_stream():
+    """Joint models: every step starts from the given text states, so a
+    two-step run equals two one-step runs that both use the original x_txt."""
+    cfg = tiny_cfg(n_blocks=1, patch_in=6, patch_out=6, batch=1, text_tokens=5)
+    sw = {k: v.astype(np.float64) for k, v in synth.step_weights(cfg).items()}
+    blocks = [{"img": weights(cfg, block=0, stream=0), "txt": weights(cfg, block=0, stream=1)}]
+    z0 = rand((1, cfg.tokens, 6), 57)
+    xt = rand((1, 5, cfg.hidden), 58)
+    c = rand((1, cfg.hidden), 59)
+    whole = O.sample_euler(cfg, z0, [1.0, 0.5, 0.0], sw, blocks, cond=c, x_txt=xt)
+    a = O.sample_euler(cfg, z0, [1.0, 0.5], sw, blocks, cond=c, x_txt=xt)
+    b = O.sample_euler(cfg, a, [0.5, 0.0], sw, blocks, cond=c, x_txt=xt)
+    assert np.array_equal(whole, b)
