@@ -66,7 +66,7 @@ typedef enum {
 typedef enum { DIT_F32 = 0, DIT_BF16 = 1 } dit_dtype;
 
 /* Workspace kinds for dit_workspace_bytes(). */
-typedef enum { DIT_WS_BLOCK = 0, DIT_WS_STEP = 1, DIT_WS_COND = 2 } dit_ws_kind;
+typedef enum { DIT_WS_BLOCK = 0, DIT_WS_STEP = 1, DIT_WS_COND = 2, DIT_WS_SAMPLE = 3 } dit_ws_kind;
 
 /* Shape of one DiT model / workload.
  *   batch         B >= 1 samples
@@ -155,6 +155,37 @@ dit_status dit_step_forward(const dit_shape *s, const dit_step_weights *w, const
 dit_status dit_cond_embed(const dit_shape *s, const float *t, const int32_t *y, const void *w_t1,
                           const void *b_t1, const void *w_t2, const void *b_t2, const void *class_table,
                           float *cond, void *workspace, size_t ws_bytes, void *stream);
+
+/* Weights of the timestep + class conditioning (see dit_cond_embed). */
+typedef struct {
+  const void *w_t1, *b_t1, *w_t2, *b_t2, *class_table;
+} dit_cond_weights;
+
+/* The DiT stage's multi-step denoising loop (paper: Background and
+ * Motivation, Workload Characteristics -- 40-50 iterations for standard
+ * samplers, 4 or 8 for distilled ones; System Design -- the Transformer
+ * service iterates the backbone over the timesteps and updates the latent).
+ * The paper names no sampler; this is first-order Euler on the
+ * flow-matching ODE in the patchified latent space:
+ *   for i in 0 .. n_steps-1:
+ *     c_i = cond_w ? class conditioning at t_i = (float)(sigmas[i] * t_scale)
+ *                    and labels y (as dit_cond_embed)
+ *                  : cond (the same for every step)
+ *     v_i = one step (dit_step_forward) on z with c_i; joint models start every
+ *           step from the given text states x_txt (which are not modified)
+ *     z  += (sigmas[i+1] - sigmas[i]) * v_i      (difference taken in fp32)
+ *   z       [B, T, P] fp32, P = patch_in = patch_out, updated in place
+ *   sigmas  HOST array of n_steps + 1 floats (any order); n_steps >= 0
+ *   cond_w  conditioning weights (class-conditioned models) with y [B] int32
+ *           device labels, or NULL with cond [B, D] fp32 given
+ *   x_txt   [B, Tt, D] fp32 text states (joint only, else NULL), read only
+ *   workspace >= dit_workspace_bytes(s, DIT_WS_SAMPLE) bytes
+ * Enqueues no allocation or memset, so the whole loop can be captured into a
+ * HIP graph and replayed.  Errors as dit_step_forward. */
+dit_status dit_sample_euler(const dit_shape *s, const dit_step_weights *w, const dit_cond_weights *cond_w,
+                            const int32_t *y, const float *cond, const float *sigmas, int32_t n_steps,
+                            float t_scale, float *z, const float *x_txt, void *workspace, size_t ws_bytes,
+                            void *stream);
 
 /* Fixed 2-D sin-cos position table of DiT, pos [grid_h*grid_w, hidden] fp32,
  * token n = r*grid_w + c: features [0, D/2) encode column c, [D/2, D) row r;

@@ -19,12 +19,12 @@ LIB_PATH = os.path.join(_HERE, "libditmi.so")
 
 DIT_OK, DIT_ERR_INVALID_ARG, DIT_ERR_UNSUPPORTED, DIT_ERR_WORKSPACE, DIT_ERR_HIP = 0, -1, -2, -3, -4
 DIT_F32, DIT_BF16 = 0, 1
-DIT_WS_BLOCK, DIT_WS_STEP, DIT_WS_COND = 0, 1, 2
+DIT_WS_BLOCK, DIT_WS_STEP, DIT_WS_COND, DIT_WS_SAMPLE = 0, 1, 2, 3
 KERNEL_CLASSES = {"gemm_qkv": 0, "attention": 1, "gemm_out": 2, "gemm_fc1": 3, "gemm_fc2": 4,
                   "ln_mod": 5, "adaln": 6, "other": 7}
 
 STREAM_FIELDS = ("w_ada", "b_ada", "w_qkv", "b_qkv", "w_o", "b_o", "w_fc1", "b_fc1", "w_fc2", "b_fc2")
-C_API = ("dit_workspace_bytes", "dit_block_forward", "dit_step_forward", "dit_cond_embed", "dit_pos_embed_2d",
+C_API = ("dit_workspace_bytes", "dit_block_forward", "dit_step_forward", "dit_sample_euler", "dit_cond_embed", "dit_pos_embed_2d",
          "dit_timing_enable", "dit_timing_read", "dit_timing_disable", "dit_status_string", "dit_last_error",
          "dit_version")
 
@@ -59,6 +59,10 @@ class StepWeights(ctypes.Structure):
 _LIB: Optional[ctypes.CDLL] = None
 
 
+class CondWeights(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in ("w_t1", "b_t1", "w_t2", "b_t2", "class_table")]
+
+
 def lib() -> ctypes.CDLL:
     """Load libditmi.so (raises if it has not been built)."""
     global _LIB
@@ -74,6 +78,8 @@ def lib() -> ctypes.CDLL:
     L.dit_block_forward.argtypes = [P(Shape), P(BlockWeights), vp, vp, vp, vp, sz, vp]
     L.dit_step_forward.argtypes = [P(Shape), P(StepWeights), vp, vp, vp, vp, vp, sz, vp]
     L.dit_cond_embed.argtypes = [P(Shape), vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+    L.dit_sample_euler.argtypes = [P(Shape), P(StepWeights), P(CondWeights), vp, vp, P(ctypes.c_float), i32,
+                                   ctypes.c_float, vp, vp, vp, sz, vp]
     L.dit_pos_embed_2d.argtypes = [i32, i32, i32, vp, vp]
     L.dit_timing_enable.argtypes = [ctypes.c_int, ctypes.c_int]
     L.dit_timing_read.argtypes = [P(ctypes.c_double), P(ctypes.c_int), P(ctypes.c_double), P(ctypes.c_double)]
@@ -190,6 +196,29 @@ def step_forward(shape: Shape, table: StepWeightTable, patches: torch.Tensor, co
     _check(lib().dit_step_forward(ctypes.byref(shape), ctypes.byref(table.struct),
                                   _ptr(patches, torch.float32, "patches"), _ptr(x_txt, torch.float32, "x_txt"),
                                   _ptr(cond, torch.float32, "cond"), _ptr(out, torch.float32, "out"),
+                                  _ptr(workspace, None, "workspace"), workspace.numel() * workspace.element_size(),
+                                  _stream(stream)))
+
+
+def sample_euler(shape: Shape, table: StepWeightTable, z: torch.Tensor, sigmas, workspace: torch.Tensor,
+                 cond_w: Optional[Dict[str, torch.Tensor]] = None, y: Optional[torch.Tensor] = None,
+                 cond: Optional[torch.Tensor] = None, t_scale: float = 1000.0,
+                 x_txt: Optional[torch.Tensor] = None, stream=None) -> None:
+    """Multi-step Euler loop over the step (z updated in place): with cond_w and
+    y the conditioning is recomputed per step at t_i = sigmas[i] * t_scale;
+    otherwise cond is used for every step.  sigmas: n_steps + 1 floats (host)."""
+    sig = [float(v) for v in sigmas]
+    if len(sig) < 1:
+        raise ValueError("sigmas needs at least one value")
+    arr = (ctypes.c_float * len(sig))(*sig)
+    cw = None
+    if cond_w is not None:
+        dt = weight_dtype(shape)
+        cw = CondWeights(*[_ptr(cond_w[k], dt, k) for k in ("w_t1", "b_t1", "w_t2", "b_t2", "class_table")])
+    _check(lib().dit_sample_euler(ctypes.byref(shape), ctypes.byref(table.struct),
+                                  ctypes.byref(cw) if cw is not None else None,
+                                  _ptr(y, torch.int32, "y"), _ptr(cond, torch.float32, "cond"), arr, len(sig) - 1,
+                                  float(t_scale), _ptr(z, torch.float32, "z"), _ptr(x_txt, torch.float32, "x_txt"),
                                   _ptr(workspace, None, "workspace"), workspace.numel() * workspace.element_size(),
                                   _stream(stream)))
 

@@ -70,6 +70,7 @@ dit_status check_shape(const dit_shape* s, bool step) {
 
 struct Layout {
   size_t mod, act, h, q, k, v, o, g, x, feat, h1, total;
+  size_t t, vel, cond, xt;  // sampler loop: timesteps [B], velocity [B,T,P], c [B,D], text states [B,Tt,D]
   size_t qk;  // q/k row length (elements)
   int ns, Tj, Tj_pad;
 };
@@ -95,7 +96,8 @@ Layout layout(const dit_shape* s, int kind) {
     return L;
   }
   const size_t rows = B * (T + Tt);
-  const size_t nmod = kind == DIT_WS_STEP ? (size_t)s->n_blocks * L.ns * B * 6 * D + B * 2 * D : L.ns * B * 6 * D;
+  const bool step = kind == DIT_WS_STEP || kind == DIT_WS_SAMPLE;
+  const size_t nmod = step ? (size_t)s->n_blocks * L.ns * B * 6 * D + B * 2 * D : L.ns * B * 6 * D;
   L.mod = take(nmod * 4);
   L.act = take((B + 15) / 16 * 16 * D * 2);  // SiLU(c) in bf16 for the adaLN MFMA kernel
   L.h = take(rows * D * E);
@@ -105,7 +107,15 @@ Layout layout(const dit_shape* s, int kind) {
   L.v = take(E == 2 ? B * H * dh * (size_t)L.Tj_pad * 2 : B * H * L.Tj * dh * 4);
   L.o = take(rows * D * E);
   L.g = take(rows * F * E);
-  L.x = kind == DIT_WS_STEP ? take(B * T * D * 4) : 0;
+  L.x = step ? take(B * T * D * 4) : 0;
+  if (kind == DIT_WS_SAMPLE) {
+    L.t = take(B * 4);
+    L.vel = take(B * T * (size_t)s->patch_out * 4);
+    L.cond = take(B * D * 4);
+    L.feat = take(B * 256 * 4);
+    L.h1 = take(B * D * 4);
+    L.xt = take(B * Tt * D * 4);
+  }
   L.total = off;
   return L;
 }
@@ -463,65 +473,9 @@ dit_status run_adaln(const dit_shape* s, const float* cond, void* act, const std
   return DIT_OK;
 }
 
-}  // namespace
-
-// ====================================================================== C ABI
-extern "C" {
-
-int dit_version(void) { return DITMI_VERSION; }
-
-const char* dit_status_string(dit_status st) {
-  switch (st) {
-    case DIT_OK: return "ok";
-    case DIT_ERR_INVALID_ARG: return "invalid argument";
-    case DIT_ERR_UNSUPPORTED: return "unsupported shape";
-    case DIT_ERR_WORKSPACE: return "workspace too small";
-    case DIT_ERR_HIP: return "HIP runtime error";
-  }
-  return "unknown status";
-}
-
-const char* dit_last_error(void) { return g_err.c_str(); }
-
-size_t dit_workspace_bytes(const dit_shape* s, int kind) {
-  if (kind != DIT_WS_BLOCK && kind != DIT_WS_STEP && kind != DIT_WS_COND) {
-    fail(DIT_ERR_INVALID_ARG, "unknown workspace kind %d", kind);
-    return 0;
-  }
-  if (check_shape(s, kind == DIT_WS_STEP) != DIT_OK) return 0;
-  return layout(s, kind).total;
-}
-
-dit_status dit_block_forward(const dit_shape* s, const dit_block_weights* w, float* x, float* x_txt,
-                             const float* cond, void* workspace, size_t ws_bytes, void* stream) {
-  dit_status st = check_shape(s, false);
-  if (st != DIT_OK) return st;
-  if (!w) return fail(DIT_ERR_INVALID_ARG, "weights is NULL");
-  if ((st = check_stream_weights(w->img, "image-stream")) != DIT_OK) return st;
-  const bool joint = s->text_tokens > 0;
-  if (joint && (st = check_stream_weights(w->txt, "text-stream")) != DIT_OK) return st;
-  if (!x || !aligned(x, 16)) return fail(DIT_ERR_INVALID_ARG, "x NULL or not 16-byte aligned");
-  if (joint && (!x_txt || !aligned(x_txt, 16))) return fail(DIT_ERR_INVALID_ARG, "x_txt NULL or not 16-byte aligned");
-  if (!joint && x_txt) return fail(DIT_ERR_INVALID_ARG, "x_txt must be NULL when text_tokens == 0");
-  if (!cond || !aligned(cond, 4)) return fail(DIT_ERR_INVALID_ARG, "cond NULL or misaligned");
-  const Layout L = layout(s, DIT_WS_BLOCK);
-  if (!workspace || !aligned(workspace, 256)) return fail(DIT_ERR_INVALID_ARG, "workspace NULL or not 256-byte aligned");
-  if (ws_bytes < L.total) return fail(DIT_ERR_WORKSPACE, "workspace %zu bytes < %zu needed", ws_bytes, L.total);
-
-  hipStream_t hs = (hipStream_t)stream;
-  char* ws = (char*)workspace;
-  float* mod = (float*)(ws + L.mod);
-  const size_t per = (size_t)s->batch * 6 * s->hidden;
-  std::vector<AdaJob> jobs;
-  jobs.push_back({w->img.w_ada, w->img.b_ada, mod, 6 * s->hidden});
-  if (joint) jobs.push_back({w->txt.w_ada, w->txt.b_ada, mod + per, 6 * s->hidden});
-  if ((st = run_adaln(s, cond, ws + L.act, jobs, hs)) != DIT_OK) return st;
-  StreamIO io[2] = {{&w->img, x, mod, s->tokens}, {&w->txt, x_txt, mod + per, s->text_tokens}};
-  return run_block(s, L, ws, io, joint ? 2 : 1, hs);
-}
-
-dit_status dit_step_forward(const dit_shape* s, const dit_step_weights* w, const float* patches, float* x_txt,
-                            const float* cond, float* out, void* workspace, size_t ws_bytes, void* stream) {
+// Validation shared by the step and the sampler loop: shape, step weights
+// and every block's weights.
+dit_status check_step_weights(const dit_shape* s, const dit_step_weights* w) {
   dit_status st = check_shape(s, true);
   if (st != DIT_OK) return st;
   if (!w || !w->blocks) return fail(DIT_ERR_INVALID_ARG, "step weights or block array is NULL");
@@ -536,17 +490,16 @@ dit_status dit_step_forward(const dit_shape* s, const dit_step_weights* w, const
     if ((st = check_stream_weights(w->blocks[l].img, "image-stream")) != DIT_OK) return st;
     if (joint && (st = check_stream_weights(w->blocks[l].txt, "text-stream")) != DIT_OK) return st;
   }
-  if (!patches || !aligned(patches, 4)) return fail(DIT_ERR_INVALID_ARG, "patches NULL or misaligned");
-  if (joint && (!x_txt || !aligned(x_txt, 16))) return fail(DIT_ERR_INVALID_ARG, "x_txt NULL or not 16-byte aligned");
-  if (!joint && x_txt) return fail(DIT_ERR_INVALID_ARG, "x_txt must be NULL when text_tokens == 0");
-  if (!cond || !aligned(cond, 4)) return fail(DIT_ERR_INVALID_ARG, "cond NULL or misaligned");
-  if (!out || !aligned(out, 16)) return fail(DIT_ERR_INVALID_ARG, "out NULL or not 16-byte aligned");
-  const Layout L = layout(s, DIT_WS_STEP);
-  if (!workspace || !aligned(workspace, 256)) return fail(DIT_ERR_INVALID_ARG, "workspace NULL or not 256-byte aligned");
-  if (ws_bytes < L.total) return fail(DIT_ERR_WORKSPACE, "workspace %zu bytes < %zu needed", ws_bytes, L.total);
+  return DIT_OK;
+}
 
-  hipStream_t hs = (hipStream_t)stream;
-  char* ws = (char*)workspace;
+// One denoising step on validated arguments (the step part of the layout L
+// of the workspace ws): adaLN for all blocks, patch embedding, blocks, final
+// layer into out.
+dit_status run_step(const dit_shape* s, const dit_step_weights* w, const Layout& L, char* ws, const float* patches,
+                    float* x_txt, const float* cond, float* out, hipStream_t hs) {
+  dit_status st = DIT_OK;
+  const bool joint = s->text_tokens > 0;
   const int B = s->batch, T = s->tokens, D = s->hidden, ns = L.ns;
   float* mod = (float*)(ws + L.mod);
   const size_t per = (size_t)B * 6 * D;
@@ -607,6 +560,132 @@ dit_status dit_step_forward(const dit_shape* s, const dit_step_weights* w, const
     p.out = out;
     G.flops = 2.0 * B * T * D * s->patch_out;
     HIP_TRY(run_gemm(G, s->dtype, hs));
+  }
+  return DIT_OK;
+}
+
+}  // namespace
+
+// ====================================================================== C ABI
+extern "C" {
+
+int dit_version(void) { return DITMI_VERSION; }
+
+const char* dit_status_string(dit_status st) {
+  switch (st) {
+    case DIT_OK: return "ok";
+    case DIT_ERR_INVALID_ARG: return "invalid argument";
+    case DIT_ERR_UNSUPPORTED: return "unsupported shape";
+    case DIT_ERR_WORKSPACE: return "workspace too small";
+    case DIT_ERR_HIP: return "HIP runtime error";
+  }
+  return "unknown status";
+}
+
+const char* dit_last_error(void) { return g_err.c_str(); }
+
+size_t dit_workspace_bytes(const dit_shape* s, int kind) {
+  if (kind != DIT_WS_BLOCK && kind != DIT_WS_STEP && kind != DIT_WS_COND && kind != DIT_WS_SAMPLE) {
+    fail(DIT_ERR_INVALID_ARG, "unknown workspace kind %d", kind);
+    return 0;
+  }
+  if (check_shape(s, kind == DIT_WS_STEP || kind == DIT_WS_SAMPLE) != DIT_OK) return 0;
+  return layout(s, kind).total;
+}
+
+dit_status dit_block_forward(const dit_shape* s, const dit_block_weights* w, float* x, float* x_txt,
+                             const float* cond, void* workspace, size_t ws_bytes, void* stream) {
+  dit_status st = check_shape(s, false);
+  if (st != DIT_OK) return st;
+  if (!w) return fail(DIT_ERR_INVALID_ARG, "weights is NULL");
+  if ((st = check_stream_weights(w->img, "image-stream")) != DIT_OK) return st;
+  const bool joint = s->text_tokens > 0;
+  if (joint && (st = check_stream_weights(w->txt, "text-stream")) != DIT_OK) return st;
+  if (!x || !aligned(x, 16)) return fail(DIT_ERR_INVALID_ARG, "x NULL or not 16-byte aligned");
+  if (joint && (!x_txt || !aligned(x_txt, 16))) return fail(DIT_ERR_INVALID_ARG, "x_txt NULL or not 16-byte aligned");
+  if (!joint && x_txt) return fail(DIT_ERR_INVALID_ARG, "x_txt must be NULL when text_tokens == 0");
+  if (!cond || !aligned(cond, 4)) return fail(DIT_ERR_INVALID_ARG, "cond NULL or misaligned");
+  const Layout L = layout(s, DIT_WS_BLOCK);
+  if (!workspace || !aligned(workspace, 256)) return fail(DIT_ERR_INVALID_ARG, "workspace NULL or not 256-byte aligned");
+  if (ws_bytes < L.total) return fail(DIT_ERR_WORKSPACE, "workspace %zu bytes < %zu needed", ws_bytes, L.total);
+
+  hipStream_t hs = (hipStream_t)stream;
+  char* ws = (char*)workspace;
+  float* mod = (float*)(ws + L.mod);
+  const size_t per = (size_t)s->batch * 6 * s->hidden;
+  std::vector<AdaJob> jobs;
+  jobs.push_back({w->img.w_ada, w->img.b_ada, mod, 6 * s->hidden});
+  if (joint) jobs.push_back({w->txt.w_ada, w->txt.b_ada, mod + per, 6 * s->hidden});
+  if ((st = run_adaln(s, cond, ws + L.act, jobs, hs)) != DIT_OK) return st;
+  StreamIO io[2] = {{&w->img, x, mod, s->tokens}, {&w->txt, x_txt, mod + per, s->text_tokens}};
+  return run_block(s, L, ws, io, joint ? 2 : 1, hs);
+}
+
+dit_status dit_step_forward(const dit_shape* s, const dit_step_weights* w, const float* patches, float* x_txt,
+                            const float* cond, float* out, void* workspace, size_t ws_bytes, void* stream) {
+  dit_status st = check_step_weights(s, w);
+  if (st != DIT_OK) return st;
+  const bool joint = s->text_tokens > 0;
+  if (!patches || !aligned(patches, 4)) return fail(DIT_ERR_INVALID_ARG, "patches NULL or misaligned");
+  if (joint && (!x_txt || !aligned(x_txt, 16))) return fail(DIT_ERR_INVALID_ARG, "x_txt NULL or not 16-byte aligned");
+  if (!joint && x_txt) return fail(DIT_ERR_INVALID_ARG, "x_txt must be NULL when text_tokens == 0");
+  if (!cond || !aligned(cond, 4)) return fail(DIT_ERR_INVALID_ARG, "cond NULL or misaligned");
+  if (!out || !aligned(out, 16)) return fail(DIT_ERR_INVALID_ARG, "out NULL or not 16-byte aligned");
+  const Layout L = layout(s, DIT_WS_STEP);
+  if (!workspace || !aligned(workspace, 256)) return fail(DIT_ERR_INVALID_ARG, "workspace NULL or not 256-byte aligned");
+  if (ws_bytes < L.total) return fail(DIT_ERR_WORKSPACE, "workspace %zu bytes < %zu needed", ws_bytes, L.total);
+  return run_step(s, w, L, (char*)workspace, patches, x_txt, cond, out, (hipStream_t)stream);
+}
+
+dit_status dit_sample_euler(const dit_shape* s, const dit_step_weights* w, const dit_cond_weights* cw,
+                            const int32_t* y, const float* cond, const float* sigmas, int32_t n_steps,
+                            float t_scale, float* z, const float* x_txt, void* workspace, size_t ws_bytes,
+                            void* stream) {
+  dit_status st = check_step_weights(s, w);
+  if (st != DIT_OK) return st;
+  const bool joint = s->text_tokens > 0;
+  if (s->patch_in != s->patch_out)
+    return fail(DIT_ERR_INVALID_ARG, "the sampler needs patch_in == patch_out (%d != %d)", s->patch_in, s->patch_out);
+  if (n_steps < 0) return fail(DIT_ERR_INVALID_ARG, "n_steps %d < 0", n_steps);
+  if (!sigmas) return fail(DIT_ERR_INVALID_ARG, "sigmas is NULL");
+  if (!z || !aligned(z, 16)) return fail(DIT_ERR_INVALID_ARG, "z NULL or not 16-byte aligned");
+  if (joint && (!x_txt || !aligned(x_txt, 16))) return fail(DIT_ERR_INVALID_ARG, "x_txt NULL or not 16-byte aligned");
+  if (!joint && x_txt) return fail(DIT_ERR_INVALID_ARG, "x_txt must be NULL when text_tokens == 0");
+  if (cw) {
+    if (!y || !cw->w_t1 || !cw->b_t1 || !cw->w_t2 || !cw->b_t2 || !cw->class_table)
+      return fail(DIT_ERR_INVALID_ARG, "a conditioning pointer (or y) is NULL");
+    if (!aligned(cw->w_t1, 16) || !aligned(cw->w_t2, 16))
+      return fail(DIT_ERR_INVALID_ARG, "w_t1 and w_t2 must be 16-byte aligned");
+  } else if (!cond || !aligned(cond, 4)) {
+    return fail(DIT_ERR_INVALID_ARG, "cond NULL or misaligned (and no conditioning weights)");
+  }
+  const Layout L = layout(s, DIT_WS_SAMPLE);
+  if (!workspace || !aligned(workspace, 256)) return fail(DIT_ERR_INVALID_ARG, "workspace NULL or not 256-byte aligned");
+  if (ws_bytes < L.total) return fail(DIT_ERR_WORKSPACE, "workspace %zu bytes < %zu needed", ws_bytes, L.total);
+
+  hipStream_t hs = (hipStream_t)stream;
+  char* ws = (char*)workspace;
+  const int B = s->batch, D = s->hidden;
+  const long nz = (long)B * s->tokens * s->patch_out;
+  float* vel = (float*)(ws + L.vel);
+  float* xt = joint ? (float*)(ws + L.xt) : nullptr;
+  for (int i = 0; i < n_steps; ++i) {
+    const float* c = cond;
+    if (cw) {  // c_i = conditioning at t_i = sigma_i * t_scale (fp32), every sample
+      const float t = sigmas[i] * t_scale;
+      HIP_TRY(launch_fill_f32((float*)(ws + L.t), B, t, hs));
+      HIP_TRY(timed(DIT_K_OTHER, 0, 0, hs, [&]() {
+        return launch_cond_embed(B, D, (const float*)(ws + L.t), y, cw->w_t1, cw->b_t1, cw->w_t2, cw->b_t2,
+                                 cw->class_table, (float*)(ws + L.feat), (float*)(ws + L.h1), (float*)(ws + L.cond),
+                                 s->dtype, hs);
+      }));
+      c = (const float*)(ws + L.cond);
+    }
+    if (joint)  // every step starts from the given text states
+      HIP_TRY(hipMemcpyAsync(xt, x_txt, (size_t)B * s->text_tokens * D * sizeof(float), hipMemcpyDeviceToDevice, hs));
+    if ((st = run_step(s, w, L, ws, z, xt, c, vel, hs)) != DIT_OK) return st;
+    const float dsig = sigmas[i + 1] - sigmas[i];
+    HIP_TRY(timed(DIT_K_OTHER, 2.0 * nz, 12.0 * nz, hs, [&]() { return launch_axpy_f32(z, vel, dsig, nz, hs); }));
   }
   return DIT_OK;
 }

@@ -415,6 +415,34 @@ hipError_t launch_pos_embed_2d(int gh, int gw, int D, float* pos, hipStream_t st
   return hipGetLastError();
 }
 
+// ---------------------------------------------------------------- sampler loop
+// p[i] = v for i < n (per-step timestep for the conditioning; a kernel, not a
+// memset, so that the loop can be captured into a HIP graph).
+__global__ void fill_f32_kernel(float* p, int n, float v) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = v;
+}
+
+hipError_t launch_fill_f32(float* p, int n, float v, hipStream_t st) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(fill_f32_kernel, dim3((n + 255) / 256), dim3(256), 0, st, p, n, v);
+  return hipGetLastError();
+}
+
+// Euler update z += a * v over n floats (n a multiple of 4, 16-byte aligned).
+__global__ void axpy_f32_kernel(f32x4* z, const f32x4* v, float a, long n4) {
+  const long i = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n4) z[i] += a * v[i];
+}
+
+hipError_t launch_axpy_f32(float* z, const float* v, float a, long n, hipStream_t st) {
+  const long n4 = n / 4;
+  if (n4 <= 0) return hipSuccess;
+  hipLaunchKernelGGL(axpy_f32_kernel, dim3((unsigned)((n4 + 255) / 256)), dim3(256), 0, st, (f32x4*)z,
+                     (const f32x4*)v, a, n4);
+  return hipGetLastError();
+}
+
 // ---------------------------------------------------------------- weight prefetch
 // Touches one dword of every 64-byte line of up to PREFETCH_MAX regions so
 // that they are resident in the memory-side Infinity Cache when the next

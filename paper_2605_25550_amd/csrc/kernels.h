@@ -110,6 +110,9 @@ hipError_t launch_patch_embed(int rows, int T, int P, int D, const float* z, con
                               const float* pos, float* x, int dtype, hipStream_t st);
 hipError_t launch_pos_embed_2d(int gh, int gw, int D, float* pos, hipStream_t st);
 hipError_t launch_prefetch(const PrefetchArgs& a, hipStream_t st);
+hipError_t launch_fill_f32(float* p, int n, float v, hipStream_t st);
+// z[i] += a * v[i], i < n; n a multiple of 4, both 16-byte aligned
+hipError_t launch_axpy_f32(float* z, const float* v, float a, long n, hipStream_t st);
 
 // Tile configurations of the bf16 GEMM (BM x BN, LDS ring depth).
 enum { TILE_128x128 = 0, TILE_64x128 = 1, TILE_64x128_S2 = 2, TILE_64x144 = 3, TILE_COUNT = 4 };

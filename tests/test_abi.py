@@ -139,6 +139,32 @@ def test_step_forward_validation(dm):
     assert call(s, nob) == -1                                    # no block array
 
 
+def test_sample_euler_validation(dm):
+    lib = dm.lib()
+    s = shape(dm, n_blocks=2)
+    blocks = (dm.BlockWeights * 2)(fake_block(dm), fake_block(dm))
+    sw = dm.StepWeights(FAKE, FAKE, None, ctypes.cast(blocks, ctypes.POINTER(dm.BlockWeights)), FAKE, FAKE, FAKE, FAKE)
+    cw = dm.CondWeights(FAKE, FAKE, FAKE, FAKE, FAKE)
+    sig = (ctypes.c_float * 3)(1.0, 0.5, 0.0)
+    need = dm.workspace_bytes(s, dm.DIT_WS_SAMPLE)
+    assert need > dm.workspace_bytes(s, dm.DIT_WS_STEP)
+
+    def call(s_=s, cw_=cw, y=FAKE, cond=None, sigmas=sig, n=2, z=FAKE, xt=None, ws_bytes=None):
+        return lib.dit_sample_euler(ctypes.byref(s_), ctypes.byref(sw), ctypes.byref(cw_) if cw_ is not None else None,
+                                    y, cond, sigmas, n, 1000.0, z, xt, FAKE, need if ws_bytes is None else ws_bytes,
+                                    None)
+
+    assert call(ws_bytes=need - 1) == -3
+    assert call(n=-1) == -1
+    assert call(sigmas=None) == -1
+    assert call(z=FAKE + 4) == -1                       # z must be 16-byte aligned
+    assert call(y=None) == -1                           # class conditioning needs labels
+    assert call(cw_=None) == -1                         # neither conditioning weights nor cond
+    assert call(cw_=dm.CondWeights(FAKE + 8, FAKE, FAKE, FAKE, FAKE)) == -1  # w_t1 misaligned
+    assert call(s_=shape(dm, n_blocks=2, patch_out=8)) == -1  # patch_in != patch_out
+    assert call(xt=FAKE) == -1                          # text states without text tokens
+
+
 def test_cond_pos_and_timing_validation(dm):
     lib = dm.lib()
     s = shape(dm)
