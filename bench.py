@@ -57,6 +57,9 @@ def parse():
                     help="no GPU work: turn two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE) of this "
                          "command with --copy-probe-mib into profiles/<kernel>_<workload>_traffic.json")
     ap.add_argument("--kernel-class", default=None, help="kernel class for --summarize-pmc")
+    ap.add_argument("--sample-steps", type=int, default=0,
+                    help="instead of single steps, time the multi-step Euler sampler loop of this many steps "
+                         "(eager and replayed from a captured HIP graph)")
     return ap.parse_args()
 
 
@@ -220,6 +223,54 @@ def cpu_baseline(cfg, n_blocks_sample: int):
                       f"({sec_per_step:.2f} s/step)"}
 
 
+def sampler_bench(wl, args, torch, dm):
+    """Denoising steps per second inside a K-step Euler sampler loop (the
+    DiT stage's per-request work), launched eagerly and replayed from a
+    captured HIP graph."""
+    cfg = wl.cfg
+    K = args.sample_steps
+    sigmas = [1.0 - i / K for i in range(K + 1)]
+    ws = dm.alloc_workspace(wl.shape, dm.DIT_WS_SAMPLE)
+    kw = {"x_txt": wl.x_txt}
+    if cfg.cond == "class":
+        kw.update(cond_w=wl.cond_w, y=wl.y)
+    else:
+        kw["cond"] = wl.cond
+    z0 = wl.patches.clone()
+    z = z0.clone()
+
+    def loop():
+        dm.sample_euler(wl.shape, wl.table, z, sigmas, ws, **kw)
+
+    loop()
+    torch.cuda.synchronize()
+    reps = max(1, args.steps // K)
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        z.copy_(z0)
+        loop()
+    torch.cuda.synchronize()
+    eager_s = (time.perf_counter() - t0) / reps
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        loop()
+    graph.replay()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        z.copy_(z0)
+        graph.replay()
+    torch.cuda.synchronize()
+    graph_s = (time.perf_counter() - t0) / reps
+    print(json.dumps({
+        "metric": f"DiT denoising steps/sec inside a {K}-step Euler sampler loop (per-step conditioning)",
+        "value": round(K / eager_s, 3), "unit": "steps/s", "n_gpus": 1, "higher_is_better": True,
+        "loop_ms": round(eager_s * 1e3, 3), "graph_value": round(K / graph_s, 3),
+        "graph_loop_ms": round(graph_s * 1e3, 3), "loops_timed": reps, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": cfg.name, "blocks": cfg.n_blocks, "batch": cfg.batch, "tokens": cfg.tokens,
+                   "sampler": "euler", "steps": K}}), flush=True)
+
+
 def main():
     args = parse()
     if args.summarize_pmc:
@@ -243,6 +294,9 @@ def main():
     dm.lib()
     wl = Workload(cfg, torch, dm)
     st = torch.cuda.current_stream()
+    if args.sample_steps:
+        sampler_bench(wl, args, torch, dm)
+        return
 
     # warmup; afterwards measure each kernel class once to find the dominant one
     for _ in range(args.warmup):
