@@ -57,6 +57,9 @@ def parse():
                     help="no GPU work: turn two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE) of this "
                          "command with --copy-probe-mib into profiles/<kernel>_<workload>_traffic.json")
     ap.add_argument("--kernel-class", default=None, help="kernel class for --summarize-pmc")
+    ap.add_argument("--serve", type=int, default=0,
+                    help="time N requests through dit_serve (copies in order vs overlapped on a second "
+                         "stream) with --sample-steps (default 1) Euler steps each")
     ap.add_argument("--sample-steps", type=int, default=0,
                     help="instead of single steps, time the multi-step Euler sampler loop of this many steps "
                          "(eager and replayed from a captured HIP graph)")
@@ -271,6 +274,62 @@ def sampler_bench(wl, args, torch, dm):
                    "sampler": "euler", "steps": K}}), flush=True)
 
 
+def serve_bench(wl, args, torch, dm):
+    """Requests through the DiT stage with host<->device latent copies in order
+    and overlapped with compute on a second stream; reports how much of the
+    copy time the overlap hides."""
+    cfg = wl.cfg
+    K = max(1, args.sample_steps)
+    N = args.serve
+    sigmas = [1.0 - i / K for i in range(K + 1)]
+    ws = dm.alloc_workspace(wl.shape, dm.DIT_WS_SERVE)
+    cond_w = wl.cond_w if cfg.cond == "class" else None
+    reqs = []
+    for i in range(N):
+        r = {"z_in": wl.patches.cpu().pin_memory(), "z_out": torch.empty_like(wl.patches, device="cpu").pin_memory()}
+        if cond_w is not None:
+            r["y"] = wl.y.cpu()
+        else:
+            r["cond"] = wl.cond.cpu()
+        reqs.append(r)
+    cs = torch.cuda.Stream()
+
+    def run(overlap):
+        dm.serve(wl.shape, wl.table, reqs, sigmas, ws, cond_w=cond_w, overlap=overlap, copy_stream=cs)
+        torch.cuda.synchronize()
+
+    def timed(fn, reps=3):
+        fn()
+        t0 = time.perf_counter()
+        for _ in range(reps):
+            fn()
+        return (time.perf_counter() - t0) / reps
+
+    serial = timed(lambda: run(False))
+    overlapped = timed(lambda: run(True))
+    zd = wl.patches.clone()
+
+    def copies():  # the same copies alone
+        for r in reqs:
+            zd.copy_(r["z_in"], non_blocking=True)
+            r["z_out"].copy_(zd, non_blocking=True)
+        torch.cuda.synchronize()
+
+    copy_s = timed(copies)
+    # the hidden share of the copy time is only resolvable when the copies are
+    # a visible part of a request's time
+    hidden = (serial - overlapped) / copy_s if copy_s > 0.05 * serial else None
+    print(json.dumps({
+        "metric": f"requests/sec through the DiT stage ({K}-step Euler loop each) with overlapped latent copies",
+        "value": round(N / overlapped, 3), "unit": "requests/s", "n_gpus": 1, "higher_is_better": True,
+        "serial_ms_per_request": round(serial / N * 1e3, 4), "overlapped_ms_per_request": round(overlapped / N * 1e3, 4),
+        "copy_only_ms_per_request": round(copy_s / N * 1e3, 4),
+        "copy_fraction_hidden": None if hidden is None else round(hidden, 3),
+        "latent_bytes_each_way": int(wl.patches.numel() * 4), "requests": N, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": cfg.name, "blocks": cfg.n_blocks, "batch": cfg.batch, "tokens": cfg.tokens,
+                   "sampler": "euler", "steps": K}}), flush=True)
+
+
 def main():
     args = parse()
     if args.summarize_pmc:
@@ -294,6 +353,9 @@ def main():
     dm.lib()
     wl = Workload(cfg, torch, dm)
     st = torch.cuda.current_stream()
+    if args.serve:
+        serve_bench(wl, args, torch, dm)
+        return
     if args.sample_steps:
         sampler_bench(wl, args, torch, dm)
         return

@@ -66,7 +66,7 @@ typedef enum {
 typedef enum { DIT_F32 = 0, DIT_BF16 = 1 } dit_dtype;
 
 /* Workspace kinds for dit_workspace_bytes(). */
-typedef enum { DIT_WS_BLOCK = 0, DIT_WS_STEP = 1, DIT_WS_COND = 2, DIT_WS_SAMPLE = 3 } dit_ws_kind;
+typedef enum { DIT_WS_BLOCK = 0, DIT_WS_STEP = 1, DIT_WS_COND = 2, DIT_WS_SAMPLE = 3, DIT_WS_SERVE = 4 } dit_ws_kind;
 
 /* Shape of one DiT model / workload.
  *   batch         B >= 1 samples
@@ -186,6 +186,41 @@ dit_status dit_sample_euler(const dit_shape *s, const dit_step_weights *w, const
                             const int32_t *y, const float *cond, const float *sigmas, int32_t n_steps,
                             float t_scale, float *z, const float *x_txt, void *workspace, size_t ws_bytes,
                             void *stream);
+
+/* One request handed to the DiT stage: host buffers (page-locked for the
+ * copies to overlap; pageable memory works but serialises) of the latent from
+ * the encoder stage, the denoised latent for the decoder stage, and the
+ * request's conditioning input. */
+typedef struct {
+  const float *z_in;      /* [B, T, P] fp32 */
+  float *z_out;           /* [B, T, P] fp32 */
+  const int32_t *y;       /* [B] labels when conditioning weights are given, else NULL */
+  const float *cond;      /* [B, D] fp32 conditioning otherwise, else NULL */
+} dit_request;
+
+/* Serve a sequence of requests through the DiT stage on one GPU: the paper's
+ * asynchronous inter-stage pipeline (System Design: the stages communicate
+ * through asynchronous queues so that requests occupy different stages at
+ * once; Challenge 1: asynchronous handoff absorbs transfer jitter) shrunk to
+ * one device.  Per request: copy z_in (and y or cond) host -> device, run the
+ * Euler loop of dit_sample_euler (same sigmas, n_steps, t_scale for every
+ * request), copy the result device -> host into z_out.
+ *   overlap != 0: the copies run on copy_stream (required) and the loops on
+ *     `stream`, with two device slots ordered by events: the input of request
+ *     i+1 and the output of request i-1 move while request i computes.
+ *   overlap == 0: everything runs in order on `stream`.
+ *   jitter_us > 0: before enqueueing each request the calling thread sleeps a
+ *     pseudo-random time in [0, jitter_us] microseconds (seeded by
+ *     jitter_seed), standing in for irregular arrivals from the encoder
+ *     stage; results do not depend on it.
+ * Results are identical for every overlap/jitter setting.  The call returns
+ * after enqueueing; synchronise `stream` before reading z_out.  Temporary
+ * HIP events are created and released by the call (no device memory).
+ *   workspace >= dit_workspace_bytes(s, DIT_WS_SERVE) bytes */
+dit_status dit_serve(const dit_shape *s, const dit_step_weights *w, const dit_cond_weights *cond_w,
+                     const dit_request *reqs, int32_t n_requests, const float *sigmas, int32_t n_steps,
+                     float t_scale, int32_t overlap, uint32_t jitter_us, uint32_t jitter_seed, void *workspace,
+                     size_t ws_bytes, void *stream, void *copy_stream);
 
 /* Fixed 2-D sin-cos position table of DiT, pos [grid_h*grid_w, hidden] fp32,
  * token n = r*grid_w + c: features [0, D/2) encode column c, [D/2, D) row r;

@@ -19,12 +19,12 @@ LIB_PATH = os.path.join(_HERE, "libditmi.so")
 
 DIT_OK, DIT_ERR_INVALID_ARG, DIT_ERR_UNSUPPORTED, DIT_ERR_WORKSPACE, DIT_ERR_HIP = 0, -1, -2, -3, -4
 DIT_F32, DIT_BF16 = 0, 1
-DIT_WS_BLOCK, DIT_WS_STEP, DIT_WS_COND, DIT_WS_SAMPLE = 0, 1, 2, 3
+DIT_WS_BLOCK, DIT_WS_STEP, DIT_WS_COND, DIT_WS_SAMPLE, DIT_WS_SERVE = 0, 1, 2, 3, 4
 KERNEL_CLASSES = {"gemm_qkv": 0, "attention": 1, "gemm_out": 2, "gemm_fc1": 3, "gemm_fc2": 4,
                   "ln_mod": 5, "adaln": 6, "other": 7}
 
 STREAM_FIELDS = ("w_ada", "b_ada", "w_qkv", "b_qkv", "w_o", "b_o", "w_fc1", "b_fc1", "w_fc2", "b_fc2")
-C_API = ("dit_workspace_bytes", "dit_block_forward", "dit_step_forward", "dit_sample_euler", "dit_cond_embed", "dit_pos_embed_2d",
+C_API = ("dit_workspace_bytes", "dit_block_forward", "dit_step_forward", "dit_sample_euler", "dit_serve", "dit_cond_embed", "dit_pos_embed_2d",
          "dit_timing_enable", "dit_timing_read", "dit_timing_disable", "dit_status_string", "dit_last_error",
          "dit_version")
 
@@ -63,6 +63,10 @@ class CondWeights(ctypes.Structure):
     _fields_ = [(n, ctypes.c_void_p) for n in ("w_t1", "b_t1", "w_t2", "b_t2", "class_table")]
 
 
+class Request(ctypes.Structure):
+    _fields_ = [("z_in", ctypes.c_void_p), ("z_out", ctypes.c_void_p), ("y", ctypes.c_void_p), ("cond", ctypes.c_void_p)]
+
+
 def lib() -> ctypes.CDLL:
     """Load libditmi.so (raises if it has not been built)."""
     global _LIB
@@ -80,6 +84,8 @@ def lib() -> ctypes.CDLL:
     L.dit_cond_embed.argtypes = [P(Shape), vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
     L.dit_sample_euler.argtypes = [P(Shape), P(StepWeights), P(CondWeights), vp, vp, P(ctypes.c_float), i32,
                                    ctypes.c_float, vp, vp, vp, sz, vp]
+    L.dit_serve.argtypes = [P(Shape), P(StepWeights), P(CondWeights), P(Request), i32, P(ctypes.c_float), i32,
+                            ctypes.c_float, i32, ctypes.c_uint32, ctypes.c_uint32, vp, sz, vp, vp]
     L.dit_pos_embed_2d.argtypes = [i32, i32, i32, vp, vp]
     L.dit_timing_enable.argtypes = [ctypes.c_int, ctypes.c_int]
     L.dit_timing_read.argtypes = [P(ctypes.c_double), P(ctypes.c_int), P(ctypes.c_double), P(ctypes.c_double)]
@@ -221,6 +227,38 @@ def sample_euler(shape: Shape, table: StepWeightTable, z: torch.Tensor, sigmas, 
                                   float(t_scale), _ptr(z, torch.float32, "z"), _ptr(x_txt, torch.float32, "x_txt"),
                                   _ptr(workspace, None, "workspace"), workspace.numel() * workspace.element_size(),
                                   _stream(stream)))
+
+
+def _host_ptr(t: Optional[torch.Tensor], dtype: torch.dtype, name: str):
+    if t is None:
+        return None
+    if not isinstance(t, torch.Tensor) or t.device.type != "cpu" or not t.is_contiguous() or t.dtype != dtype:
+        raise ValueError(f"{name} must be a contiguous host {dtype} tensor")
+    return t.data_ptr()
+
+
+def serve(shape: Shape, table: StepWeightTable, requests, sigmas, workspace: torch.Tensor,
+          cond_w: Optional[Dict[str, torch.Tensor]] = None, t_scale: float = 1000.0, overlap: bool = True,
+          jitter_us: int = 0, jitter_seed: int = 0, stream=None, copy_stream=None) -> None:
+    """Run requests through the DiT stage with copy/compute overlap.  requests:
+    list of dicts with host tensors z_in, z_out ([B,T,P] fp32, ideally pinned)
+    and y ([B] int32, with cond_w) or cond ([B,D] fp32).  Returns after
+    enqueueing; synchronise the stream before reading z_out."""
+    sig = [float(v) for v in sigmas]
+    arr = (ctypes.c_float * len(sig))(*sig)
+    reqs = (Request * max(1, len(requests)))()
+    for i, r in enumerate(requests):
+        reqs[i] = Request(_host_ptr(r["z_in"], torch.float32, "z_in"), _host_ptr(r["z_out"], torch.float32, "z_out"),
+                          _host_ptr(r.get("y"), torch.int32, "y"), _host_ptr(r.get("cond"), torch.float32, "cond"))
+    cw = None
+    if cond_w is not None:
+        dt = weight_dtype(shape)
+        cw = CondWeights(*[_ptr(cond_w[k], dt, k) for k in ("w_t1", "b_t1", "w_t2", "b_t2", "class_table")])
+    cs = copy_stream.cuda_stream if copy_stream is not None else None
+    _check(lib().dit_serve(ctypes.byref(shape), ctypes.byref(table.struct), ctypes.byref(cw) if cw is not None else None,
+                           reqs, len(requests), arr, len(sig) - 1, float(t_scale), 1 if overlap else 0, int(jitter_us),
+                           int(jitter_seed), _ptr(workspace, None, "workspace"),
+                           workspace.numel() * workspace.element_size(), _stream(stream), cs))
 
 
 def cond_embed(shape: Shape, t: torch.Tensor, y: torch.Tensor, w: Dict[str, torch.Tensor], cond: torch.Tensor,

@@ -10,7 +10,9 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <chrono>
 #include <mutex>
+#include <thread>
 #include <string>
 #include <vector>
 
@@ -71,6 +73,7 @@ dit_status check_shape(const dit_shape* s, bool step) {
 struct Layout {
   size_t mod, act, h, q, k, v, o, g, x, feat, h1, total;
   size_t t, vel, cond, xt;  // sampler loop: timesteps [B], velocity [B,T,P], c [B,D], text states [B,Tt,D]
+  size_t slot_z[2], slot_y[2], slot_c[2];  // serving: two request slots
   size_t qk;  // q/k row length (elements)
   int ns, Tj, Tj_pad;
 };
@@ -96,7 +99,7 @@ Layout layout(const dit_shape* s, int kind) {
     return L;
   }
   const size_t rows = B * (T + Tt);
-  const bool step = kind == DIT_WS_STEP || kind == DIT_WS_SAMPLE;
+  const bool step = kind == DIT_WS_STEP || kind == DIT_WS_SAMPLE || kind == DIT_WS_SERVE;
   const size_t nmod = step ? (size_t)s->n_blocks * L.ns * B * 6 * D + B * 2 * D : L.ns * B * 6 * D;
   L.mod = take(nmod * 4);
   L.act = take((B + 15) / 16 * 16 * D * 2);  // SiLU(c) in bf16 for the adaLN MFMA kernel
@@ -108,7 +111,7 @@ Layout layout(const dit_shape* s, int kind) {
   L.o = take(rows * D * E);
   L.g = take(rows * F * E);
   L.x = step ? take(B * T * D * 4) : 0;
-  if (kind == DIT_WS_SAMPLE) {
+  if (kind == DIT_WS_SAMPLE || kind == DIT_WS_SERVE) {
     L.t = take(B * 4);
     L.vel = take(B * T * (size_t)s->patch_out * 4);
     L.cond = take(B * D * 4);
@@ -116,6 +119,12 @@ Layout layout(const dit_shape* s, int kind) {
     L.h1 = take(B * D * 4);
     L.xt = take(B * Tt * D * 4);
   }
+  if (kind == DIT_WS_SERVE)
+    for (int k = 0; k < 2; ++k) {
+      L.slot_z[k] = take(B * T * (size_t)s->patch_out * 4);
+      L.slot_y[k] = take(B * 4);
+      L.slot_c[k] = take(B * D * 4);
+    }
   L.total = off;
   return L;
 }
@@ -564,6 +573,40 @@ dit_status run_step(const dit_shape* s, const dit_step_weights* w, const Layout&
   return DIT_OK;
 }
 
+// The Euler loop of dit_sample_euler on validated arguments (sampler part of
+// the layout L of ws): per step the conditioning (from cw and y at
+// t_i = sigma_i * t_scale, or the given cond), the step into the velocity
+// buffer, and z += (sigma_{i+1} - sigma_i) v.
+dit_status run_sample_loop(const dit_shape* s, const dit_step_weights* w, const dit_cond_weights* cw,
+                           const int32_t* y, const float* cond, const float* sigmas, int n_steps, float t_scale,
+                           float* z, const float* x_txt, const Layout& L, char* ws, hipStream_t hs) {
+  dit_status st = DIT_OK;
+  const bool joint = s->text_tokens > 0;
+  const int B = s->batch, D = s->hidden;
+  const long nz = (long)B * s->tokens * s->patch_out;
+  float* vel = (float*)(ws + L.vel);
+  float* xt = joint ? (float*)(ws + L.xt) : nullptr;
+  for (int i = 0; i < n_steps; ++i) {
+    const float* c = cond;
+    if (cw) {  // c_i = conditioning at t_i = sigma_i * t_scale (fp32), every sample
+      const float t = sigmas[i] * t_scale;
+      HIP_TRY(launch_fill_f32((float*)(ws + L.t), B, t, hs));
+      HIP_TRY(timed(DIT_K_OTHER, 0, 0, hs, [&]() {
+        return launch_cond_embed(B, D, (const float*)(ws + L.t), y, cw->w_t1, cw->b_t1, cw->w_t2, cw->b_t2,
+                                 cw->class_table, (float*)(ws + L.feat), (float*)(ws + L.h1), (float*)(ws + L.cond),
+                                 s->dtype, hs);
+      }));
+      c = (const float*)(ws + L.cond);
+    }
+    if (joint)  // every step starts from the given text states
+      HIP_TRY(hipMemcpyAsync(xt, x_txt, (size_t)B * s->text_tokens * D * sizeof(float), hipMemcpyDeviceToDevice, hs));
+    if ((st = run_step(s, w, L, ws, z, xt, c, vel, hs)) != DIT_OK) return st;
+    const float dsig = sigmas[i + 1] - sigmas[i];
+    HIP_TRY(timed(DIT_K_OTHER, 2.0 * nz, 12.0 * nz, hs, [&]() { return launch_axpy_f32(z, vel, dsig, nz, hs); }));
+  }
+  return DIT_OK;
+}
+
 }  // namespace
 
 // ====================================================================== C ABI
@@ -585,11 +628,11 @@ const char* dit_status_string(dit_status st) {
 const char* dit_last_error(void) { return g_err.c_str(); }
 
 size_t dit_workspace_bytes(const dit_shape* s, int kind) {
-  if (kind != DIT_WS_BLOCK && kind != DIT_WS_STEP && kind != DIT_WS_COND && kind != DIT_WS_SAMPLE) {
+  if (kind < DIT_WS_BLOCK || kind > DIT_WS_SERVE) {
     fail(DIT_ERR_INVALID_ARG, "unknown workspace kind %d", kind);
     return 0;
   }
-  if (check_shape(s, kind == DIT_WS_STEP || kind == DIT_WS_SAMPLE) != DIT_OK) return 0;
+  if (check_shape(s, kind == DIT_WS_STEP || kind == DIT_WS_SAMPLE || kind == DIT_WS_SERVE) != DIT_OK) return 0;
   return layout(s, kind).total;
 }
 
@@ -637,6 +680,84 @@ dit_status dit_step_forward(const dit_shape* s, const dit_step_weights* w, const
   return run_step(s, w, L, (char*)workspace, patches, x_txt, cond, out, (hipStream_t)stream);
 }
 
+dit_status dit_serve(const dit_shape* s, const dit_step_weights* w, const dit_cond_weights* cw,
+                     const dit_request* reqs, int32_t n_requests, const float* sigmas, int32_t n_steps, float t_scale,
+                     int32_t overlap, uint32_t jitter_us, uint32_t jitter_seed, void* workspace, size_t ws_bytes,
+                     void* stream, void* copy_stream) {
+  if (s && s->text_tokens > 0)
+    return fail(DIT_ERR_UNSUPPORTED, "dit_serve handles image-only models (text_tokens == 0)");
+  dit_status st = check_step_weights(s, w);
+  if (st != DIT_OK) return st;
+  if (s->patch_in != s->patch_out)
+    return fail(DIT_ERR_INVALID_ARG, "the sampler needs patch_in == patch_out (%d != %d)", s->patch_in, s->patch_out);
+  if (n_requests < 0 || n_steps < 0) return fail(DIT_ERR_INVALID_ARG, "negative request or step count");
+  if (n_requests > 0 && (!reqs || !sigmas)) return fail(DIT_ERR_INVALID_ARG, "reqs or sigmas is NULL");
+  if (overlap && !copy_stream) return fail(DIT_ERR_INVALID_ARG, "overlap needs a copy stream");
+  if (cw && (!cw->w_t1 || !cw->b_t1 || !cw->w_t2 || !cw->b_t2 || !cw->class_table))
+    return fail(DIT_ERR_INVALID_ARG, "a conditioning weight pointer is NULL");
+  if (cw && (!aligned(cw->w_t1, 16) || !aligned(cw->w_t2, 16)))
+    return fail(DIT_ERR_INVALID_ARG, "w_t1 and w_t2 must be 16-byte aligned");
+  for (int i = 0; i < n_requests; ++i) {
+    if (!reqs[i].z_in || !reqs[i].z_out) return fail(DIT_ERR_INVALID_ARG, "request %d: z_in or z_out is NULL", i);
+    if (cw ? !reqs[i].y : !reqs[i].cond)
+      return fail(DIT_ERR_INVALID_ARG, "request %d: %s is NULL", i, cw ? "y" : "cond");
+  }
+  const Layout L = layout(s, DIT_WS_SERVE);
+  if (!workspace || !aligned(workspace, 256)) return fail(DIT_ERR_INVALID_ARG, "workspace NULL or not 256-byte aligned");
+  if (ws_bytes < L.total) return fail(DIT_ERR_WORKSPACE, "workspace %zu bytes < %zu needed", ws_bytes, L.total);
+  if (n_requests == 0) return DIT_OK;
+
+  hipStream_t hs = (hipStream_t)stream;
+  hipStream_t cs = overlap ? (hipStream_t)copy_stream : hs;
+  char* ws = (char*)workspace;
+  const int B = s->batch, D = s->hidden;
+  const size_t zb = (size_t)B * s->tokens * s->patch_out * sizeof(float);
+  // ev_in[k]: inputs of the request in slot k are on the device;
+  // ev_done[k]: its loop finished; ev_free[k]: its output left the device.
+  hipEvent_t ev[6] = {};
+  for (hipEvent_t& e : ev) HIP_TRY(hipEventCreateWithFlags(&e, hipEventDisableTiming));
+  hipEvent_t *ev_in = ev, *ev_done = ev + 2, *ev_free = ev + 4;
+  dit_status result = DIT_OK;
+  uint32_t rng = jitter_seed * 2654435761u + 1u;
+  auto jitter = [&]() {
+    if (!jitter_us) return;
+    rng ^= rng << 13; rng ^= rng >> 17; rng ^= rng << 5;  // xorshift32
+    std::this_thread::sleep_for(std::chrono::microseconds(rng % (jitter_us + 1)));
+  };
+  auto fetch = [&](int i) -> hipError_t {  // host -> device slot of request i (on cs)
+    const int k = i & 1;
+    hipError_t e = hipSuccess;
+    if (i >= 2) e = hipStreamWaitEvent(cs, ev_free[k], 0);  // slot's previous output has left
+    if (e == hipSuccess) e = hipMemcpyAsync(ws + L.slot_z[k], reqs[i].z_in, zb, hipMemcpyHostToDevice, cs);
+    if (e == hipSuccess)
+      e = cw ? hipMemcpyAsync(ws + L.slot_y[k], reqs[i].y, (size_t)B * sizeof(int32_t), hipMemcpyHostToDevice, cs)
+             : hipMemcpyAsync(ws + L.slot_c[k], reqs[i].cond, (size_t)B * D * sizeof(float), hipMemcpyHostToDevice, cs);
+    if (e == hipSuccess) e = hipEventRecord(ev_in[k], cs);
+    return e;
+  };
+  hipError_t e = fetch(0);
+  for (int i = 0; i < n_requests && e == hipSuccess && result == DIT_OK; ++i) {
+    const int k = i & 1;
+    jitter();
+    e = hipStreamWaitEvent(hs, ev_in[k], 0);
+    if (e != hipSuccess) break;
+    result = run_sample_loop(s, w, cw, (const int32_t*)(ws + L.slot_y[k]), (const float*)(ws + L.slot_c[k]), sigmas,
+                             n_steps, t_scale, (float*)(ws + L.slot_z[k]), nullptr, L, ws, hs);
+    if (result != DIT_OK) break;
+    e = hipEventRecord(ev_done[k], hs);
+    if (e == hipSuccess && i + 1 < n_requests) e = fetch(i + 1);  // next input moves while request i computes
+    if (e == hipSuccess) e = hipStreamWaitEvent(cs, ev_done[k], 0);
+    if (e == hipSuccess) e = hipMemcpyAsync(reqs[i].z_out, ws + L.slot_z[k], zb, hipMemcpyDeviceToHost, cs);
+    if (e == hipSuccess) e = hipEventRecord(ev_free[k], cs);
+  }
+  // the caller's stream waits for the last copies; the events can then go
+  if (e == hipSuccess && result == DIT_OK && overlap) e = hipStreamWaitEvent(hs, ev_free[(n_requests - 1) & 1], 0);
+  for (hipEvent_t& x : ev) (void)hipEventDestroy(x);
+  if (result != DIT_OK) return result;
+  if (e != hipSuccess) return fail(DIT_ERR_HIP, "dit_serve: %s", hipGetErrorString(e));
+  return DIT_OK;
+}
+
 dit_status dit_sample_euler(const dit_shape* s, const dit_step_weights* w, const dit_cond_weights* cw,
                             const int32_t* y, const float* cond, const float* sigmas, int32_t n_steps,
                             float t_scale, float* z, const float* x_txt, void* workspace, size_t ws_bytes,
@@ -663,31 +784,8 @@ dit_status dit_sample_euler(const dit_shape* s, const dit_step_weights* w, const
   if (!workspace || !aligned(workspace, 256)) return fail(DIT_ERR_INVALID_ARG, "workspace NULL or not 256-byte aligned");
   if (ws_bytes < L.total) return fail(DIT_ERR_WORKSPACE, "workspace %zu bytes < %zu needed", ws_bytes, L.total);
 
-  hipStream_t hs = (hipStream_t)stream;
-  char* ws = (char*)workspace;
-  const int B = s->batch, D = s->hidden;
-  const long nz = (long)B * s->tokens * s->patch_out;
-  float* vel = (float*)(ws + L.vel);
-  float* xt = joint ? (float*)(ws + L.xt) : nullptr;
-  for (int i = 0; i < n_steps; ++i) {
-    const float* c = cond;
-    if (cw) {  // c_i = conditioning at t_i = sigma_i * t_scale (fp32), every sample
-      const float t = sigmas[i] * t_scale;
-      HIP_TRY(launch_fill_f32((float*)(ws + L.t), B, t, hs));
-      HIP_TRY(timed(DIT_K_OTHER, 0, 0, hs, [&]() {
-        return launch_cond_embed(B, D, (const float*)(ws + L.t), y, cw->w_t1, cw->b_t1, cw->w_t2, cw->b_t2,
-                                 cw->class_table, (float*)(ws + L.feat), (float*)(ws + L.h1), (float*)(ws + L.cond),
-                                 s->dtype, hs);
-      }));
-      c = (const float*)(ws + L.cond);
-    }
-    if (joint)  // every step starts from the given text states
-      HIP_TRY(hipMemcpyAsync(xt, x_txt, (size_t)B * s->text_tokens * D * sizeof(float), hipMemcpyDeviceToDevice, hs));
-    if ((st = run_step(s, w, L, ws, z, xt, c, vel, hs)) != DIT_OK) return st;
-    const float dsig = sigmas[i + 1] - sigmas[i];
-    HIP_TRY(timed(DIT_K_OTHER, 2.0 * nz, 12.0 * nz, hs, [&]() { return launch_axpy_f32(z, vel, dsig, nz, hs); }));
-  }
-  return DIT_OK;
+  return run_sample_loop(s, w, cw, y, cond, sigmas, n_steps, t_scale, z, x_txt, L, (char*)workspace,
+                         (hipStream_t)stream);
 }
 
 dit_status dit_cond_embed(const dit_shape* s, const float* t, const int32_t* y, const void* w_t1, const void* b_t1,

@@ -165,6 +165,32 @@ def test_sample_euler_validation(dm):
     assert call(xt=FAKE) == -1                          # text states without text tokens
 
 
+def test_serve_validation(dm):
+    lib = dm.lib()
+    s = shape(dm, n_blocks=2)
+    blocks = (dm.BlockWeights * 2)(fake_block(dm), fake_block(dm))
+    sw = dm.StepWeights(FAKE, FAKE, None, ctypes.cast(blocks, ctypes.POINTER(dm.BlockWeights)), FAKE, FAKE, FAKE, FAKE)
+    cw = dm.CondWeights(FAKE, FAKE, FAKE, FAKE, FAKE)
+    sig = (ctypes.c_float * 2)(1.0, 0.0)
+    reqs = (dm.Request * 2)(dm.Request(FAKE, FAKE, FAKE, None), dm.Request(FAKE, FAKE, FAKE, None))
+    need = dm.workspace_bytes(s, dm.DIT_WS_SERVE)
+    assert need > dm.workspace_bytes(s, dm.DIT_WS_SAMPLE)
+
+    def call(s_=s, cw_=cw, r=reqs, n=2, overlap=1, cs=FAKE, ws_bytes=None):
+        return lib.dit_serve(ctypes.byref(s_), ctypes.byref(sw), ctypes.byref(cw_) if cw_ is not None else None, r, n,
+                             sig, 1, 1000.0, overlap, 0, 0, FAKE, need if ws_bytes is None else ws_bytes, None, cs)
+
+    assert call(ws_bytes=need - 1) == -3
+    assert call(cs=None) == -1                                          # overlap needs a copy stream
+    assert call(cw_=None) == -1                                         # requests carry y but no cond
+    assert call(r=None) == -1
+    assert call(n=-1) == -1
+    assert call(n=0, r=None, overlap=0, cs=None) == 0                   # nothing to do, nothing enqueued
+    joint = shape(dm, "c3", n_blocks=2)
+    assert lib.dit_serve(ctypes.byref(joint), ctypes.byref(sw), None, reqs, 2, sig, 1, 1000.0, 0, 0, 0, FAKE, 1 << 40,
+                         None, None) == -2                              # image-only models
+
+
 def test_cond_pos_and_timing_validation(dm):
     lib = dm.lib()
     s = shape(dm)

@@ -275,3 +275,39 @@ def test_sample_euler_graph_replay():
         torch.cuda.synchronize()
         assert torch.equal(z_static, z_eager), f"replay {r} differs from the eager loop"
         del junk
+
+
+# ------------------------------------------------------------------ serving with copy/compute overlap
+def test_serve_overlap_and_jitter_do_not_change_results():
+    """Five requests through dit_serve: in order on one stream, with the
+    copies overlapped on a second stream, and with host-side arrival jitter,
+    the outputs are bitwise identical, and each equals dit_sample_euler run on
+    that request alone (which the sampler tests pin to the oracle)."""
+    name, cfg, sigmas = SAMPLE_CASES[1]
+    g, dm, sw, blocks, inp, ds, ws_sample, kw = _sample_setup(cfg)
+    ws = dm.alloc_workspace(ds.shape, dm.DIT_WS_SERVE)
+    cond_w = kw["cond_w"]
+    reqs = []
+    for i in range(5):
+        r = synth.inputs(cfg, salt=i + 1)
+        reqs.append({"z_in": torch.from_numpy(r["patches"].astype(np.float32)).pin_memory(),
+                     "y": torch.from_numpy(r["y"].astype(np.int32)),
+                     "z_out": torch.empty(r["patches"].shape, dtype=torch.float32).pin_memory()})
+    outs = {}
+    copy_stream = torch.cuda.Stream()
+    for mode, (overlap, jitter) in {"serial": (False, 0), "overlap": (True, 0), "overlap_jitter": (True, 400)}.items():
+        for r in reqs:
+            r["z_out"].fill_(float("nan"))
+        dm.serve(ds.shape, ds.table, reqs, sigmas, ws, cond_w=cond_w, overlap=overlap, jitter_us=jitter, jitter_seed=7,
+                 copy_stream=copy_stream)
+        torch.cuda.synchronize()
+        outs[mode] = [r["z_out"].clone() for r in reqs]
+        print(f"[serve] {mode}: done", flush=True)
+    for mode in ("overlap", "overlap_jitter"):
+        for i in range(5):
+            assert torch.equal(outs[mode][i], outs["serial"][i]), (mode, i)
+    for i, r in enumerate(reqs):
+        z = r["z_in"].cuda()
+        dm.sample_euler(ds.shape, ds.table, z, sigmas, ws_sample, cond_w=cond_w, y=r["y"].cuda())
+        torch.cuda.synchronize()
+        assert torch.equal(z.cpu(), outs["serial"][i]), i
