@@ -3,10 +3,11 @@
 //   y[M, N] = A[M, K] * W[N, K]^T + bias,  fp32 accumulate,
 // followed by a fused epilogue (kernels.h: Epi).
 //
-// Both operands are K-contiguous.  A workgroup of 4 waves (2 x 2) owns a
-// BM x BN tile; each wave owns (BM/2) x (BN/2) as 32x32 accumulators of
-// v_mfma_f32_32x32x16_bf16, whose lanes each read 8 consecutive bf16 of one
-// row from LDS.
+// Both operands are K-contiguous.  A workgroup of WGM x WGN waves owns a
+// BM x BN tile (4 waves for 128- and 64-row tiles, 8 waves, two per SIMD, for
+// 256-row tiles); each wave owns (BM/WGM) x (BN/WGN) as 32x32 accumulators
+// of v_mfma_f32_32x32x16_bf16, whose lanes each read 8 consecutive bf16 of
+// one row from LDS.
 //
 // Memory pipeline.  K is consumed in 64-wide slices (128 bytes per row, one
 // full cache line).  Each slice of A and W is copied HBM -> LDS by the
@@ -16,7 +17,10 @@
 // fixed 32-bit per-lane offset, so the loop spends no vector ALU work on
 // addresses.  A slot is refilled as soon as every wave has read its last
 // fragments (before the last k-step's MFMAs), so STAGES - 1 slices are in
-// flight while one is consumed.  Rows cannot be padded (the DMA writes 16
+// flight while one is consumed; the refill's DMA instructions are placed one
+// after each MFMA of two k-steps rather than issued as one burst, because the
+// address unit takes 16 cycles per 1 KB instruction and a wave waiting to
+// issue DMA cannot issue MFMAs.  Rows cannot be padded (the DMA writes 16
 // bytes per lane at consecutive LDS addresses); instead the 16-byte chunk c
 // of row r is stored at position c ^ f(r), f(r) = (r & 7) ^ ((r >> 3) & 1),
 // which keeps the 16 rows read by one quarter-wavefront on distinct banks.
@@ -33,22 +37,29 @@
 
 namespace ditmi {
 
-template <int BM, int BN, int STAGES>
+template <int BM, int BN, int WGM, int WGN, int STAGES>
 struct GemmCfg {
+  static constexpr int NW = WGM * WGN;          // waves per workgroup (WGM along M, WGN along N)
   static constexpr int BK = 64;                 // K per slice (128 bytes per row)
-  static constexpr int WTM = BM / 2, WTN = BN / 2;
+  static constexpr int WTM = BM / WGM, WTN = BN / WGN;
   static constexpr int TM = WTM / 32, TN = WTN / 32;
   static constexpr int ROWS = BM + BN;          // A rows then W rows in a slice buffer
   static constexpr int SLICE = ROWS * 128;      // bytes per slice buffer
-  static constexpr int IPW = ROWS / 32;         // DMA instructions (8 rows each) per wave per slice
-  static constexpr int IPW_A = BM / 32;         // ... of which read A
+  static constexpr int IPW = ROWS / (8 * NW);   // DMA instructions (8 rows each) per wave per slice
+  static constexpr int IPW_A = BM / (8 * NW);   // ... of which read A
   static constexpr int CST = WTN + 4;           // fp32 row stride of an epilogue slab
   static constexpr int LDS_MAIN = STAGES * SLICE;
-  static constexpr int LDS_EPI = 4 * 32 * CST * 4;
+  static constexpr int LDS_EPI = NW * 32 * CST * 4;
   static constexpr int LDS = LDS_MAIN > LDS_EPI ? LDS_MAIN : LDS_EPI;
-  static_assert(BM % 64 == 0 && BN % 64 == 0, "wave tiles are multiples of 32");
+  static_assert(WTM % 32 == 0 && WTN % 32 == 0, "wave tiles are multiples of 32");
+  static_assert(NW % 2 == 0 && ROWS % (8 * NW) == 0 && BM % (8 * NW) == 0, "uniform DMA split");
   static_assert(STAGES >= 2 && (STAGES - 1) * IPW < 64, "vmcnt range");
+  static_assert(LDS <= 160 * 1024, "LDS per CU");
 };
+
+// Orders one wave's LDS accesses across its lanes for the compiler (the
+// hardware already executes a wave's LDS instructions in order).
+__device__ __forceinline__ void wave_lds_fence() { __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront"); }
 
 // Stored position of 16-byte chunk c of slice row r.
 __device__ __forceinline__ int chunk_pos(int r, int c) { return c ^ ((r & 7) ^ ((r >> 3) & 1)); }
@@ -62,88 +73,153 @@ __device__ __forceinline__ void dma_16s(const void* sbase, unsigned voff, unsign
                : "memory", "m0");
 }
 
-// Epilogue of one LDS-staged slab of fp32 accumulators: 32 rows starting at
-// global row mb, WTN columns starting at global column nw0, row stride CST.
-// Each lane takes four consecutive columns of one row (or, for the v part of
-// the QKV projection, one column and four consecutive rows) and applies the
-// fused epilogue with 8- or 16-byte global accesses.
+// Fused epilogue of one wave's strip of WTN columns, applied one 32-row slab
+// at a time from fp32 accumulators staged in LDS (row stride CST).  Each lane
+// takes four consecutive columns of one row (or, for the v part of the QKV
+// projection, one column and four consecutive rows) and uses 8- or 16-byte
+// global accesses.  Nothing it reads from global memory is waited for at the
+// point of use: the bias (and the gate of the strip's first sample) is
+// requested when the kernel starts, and the residual rows of a slab are
+// requested before the previous slab is processed, so a slab does not expose
+// a memory round trip.
 template <int EPI, int WTN, int CST>
-__device__ __forceinline__ void epilogue_slab(const GemmProb& P, const float* Cw, int mb, int nw0, bool vcols,
-                                              int lane) {
-  const bf16_t* __restrict__ bias = (const bf16_t*)P.bias;
-  const int rpb = P.rows_per_batch, M = P.M, N = P.N;
-  const float inv_rpb = 1.0f / (float)rpb;  // wave-uniform, for div_exact
-  const float inv_dh = 1.0f / (float)P.head_dim, inv_D = 1.0f / (float)P.hidden;
-  constexpr int PER_LANE = 32 * WTN / 4 / 64;  // 4-element groups per lane per slab
+struct Epilogue {
+  static constexpr int PL = 32 * WTN / 256;  // 4-element groups per lane per slab
+  static constexpr int CPR = WTN / 4;        // 4-column groups per slab row
+  static constexpr bool RES = EPI == EPI_RESID || EPI == EPI_RESID2;
+  static constexpr int NX = RES ? PL : 1;
+  // A lane's column group in iteration it is (lane + 64 it) % CPR, which
+  // takes NCG distinct values (NCG = 1 when CPR divides 64).
+  static constexpr int gcd(int a, int b) { return b == 0 ? a : gcd(b, a % b); }
+  static constexpr int NCG = CPR / gcd(64, CPR);
   static_assert(32 * WTN % 256 == 0, "slab must split evenly over 64 lanes");
-  if (vcols) {
-    // v^T[b][h][d][j]: lane takes one column and four consecutive rows.
-    const int D = P.hidden, dh = P.head_dim;
+  f32x4 bias4[NCG];           // bias of the lane's column groups (row path)
+  float vb[EPI == EPI_QKV ? PL : 1];  // v path: bias of the column of each group
+  f32x4 gate4[RES ? NCG : 1]; // EPI_RESID: gate of sample b0 for the lane's column groups
+  int b0;
+
+  __device__ __forceinline__ void init(const GemmProb& P, int nw0, int mfirst, bool vcols, int lane) {
+    const bf16_t* __restrict__ bias = (const bf16_t*)P.bias;
+    const int N = P.N;
+    if (EPI == EPI_QKV && vcols) {
 #pragma unroll
-    for (int it = 0; it < PER_LANE; ++it) {
-      const int c = lane + 64 * it;
-      const int col = c >> 3, r4 = (c & 7) * 4;
-      const int n = nw0 + col, m = mb + r4;
-      if (n >= N || m >= M) continue;
-      const int rem = n - 2 * D, h = div_exact(rem, dh, inv_dh), d = rem - h * dh;
-      const float bv = bf2f(bias[n]);
-      const int b = div_exact(m, rpb, inv_rpb), jp = m - b * rpb + P.seq_off;
-      const float v0 = Cw[(r4 + 0) * CST + col] + bv, v1 = Cw[(r4 + 1) * CST + col] + bv;
-      const float v2 = Cw[(r4 + 2) * CST + col] + bv, v3 = Cw[(r4 + 3) * CST + col] + bv;
-      if (m + 3 < M && jp - P.seq_off + 3 < rpb && (jp & 3) == 0) {
-        bf16_t* vt = (bf16_t*)P.v + (((long)b * P.heads + h) * dh + d) * P.Tj_pad + jp;
-        *(u32x2*)vt = u32x2{pack_bf16x2(v0, v1), pack_bf16x2(v2, v3)};
-      } else {
-        const float vv[4] = {v0, v1, v2, v3};
-        for (int e = 0; e < 4 && m + e < M; ++e) {
-          const int be = div_exact(m + e, rpb, inv_rpb), je = (m + e) - be * rpb + P.seq_off;
-          ((bf16_t*)P.v)[(((long)be * P.heads + h) * dh + d) * P.Tj_pad + je] = f2bf(vv[e]);
-        }
+      for (int it = 0; it < PL; ++it) {
+        const int n = nw0 + (lane >> 3) + 8 * it;
+        vb[it] = n < N ? bf2f(bias[n]) : 0.f;
       }
     }
-    return;
-  }
-  constexpr int CPR = WTN / 4;  // 4-column groups per slab row
+    if (RES) {
+      const int rpb = P.rows_per_batch;
+      b0 = div_exact(min(mfirst, P.M - 1), rpb, 1.0f / (float)rpb);
+    }
 #pragma unroll
-  for (int it = 0; it < PER_LANE; ++it) {
-    const int c = lane + 64 * it;
-    const int row = c / CPR, c4 = (c % CPR) * 4;
-    const int m = mb + row, n = nw0 + c4;
-    if (m >= M || n >= N) continue;  // N is a multiple of 4
-    const f32x4 y = *(const f32x4*)&Cw[row * CST + c4];
-    const u32x2 bw2 = *(const u32x2*)(bias + n);
-    const float y0 = y[0] + __uint_as_float(bw2[0] << 16), y1 = y[1] + __uint_as_float(bw2[0] & 0xFFFF0000u);
-    const float y2 = y[2] + __uint_as_float(bw2[1] << 16), y3 = y[3] + __uint_as_float(bw2[1] & 0xFFFF0000u);
-    if (EPI == EPI_RESID || EPI == EPI_RESID2) {
-      const int b = div_exact(m, rpb, inv_rpb);
-      f32x4* xr = (f32x4*)(P.resid + (long)m * N + n);
-      const f32x4 gt = *(const f32x4*)(P.gate + (long)b * P.gate_stride + n);
-      f32x4 xv = *xr;
-      xv[0] += gt[0] * y0;
-      xv[1] += gt[1] * y1;
-      xv[2] += gt[2] * y2;
-      xv[3] += gt[3] * y3;
-      *xr = xv;
-    } else if (EPI == EPI_GELU) {
-      *(u32x2*)((bf16_t*)P.out + (long)m * N + n) =
-          u32x2{pack_bf16x2(gelu_tanh(y0), gelu_tanh(y1)), pack_bf16x2(gelu_tanh(y2), gelu_tanh(y3))};
-    } else if (EPI == EPI_STORE) {
-      *(f32x4*)((float*)P.out + (long)m * N + n) = f32x4{y0, y1, y2, y3};
-    } else {  // EPI_QKV, q and k columns: 4 consecutive d of one head
-      const int D = P.hidden, dh = P.head_dim;
-      const int s = div_exact(n, D, inv_D), rem = n - s * D, h = div_exact(rem, dh, inv_dh), d = rem - h * dh;
-      const int b = div_exact(m, rpb, inv_rpb), jp = m - b * rpb + P.seq_off;
-      bf16_t* dst = (bf16_t*)(s == 0 ? P.q : P.k) + (((long)b * P.heads + h) * P.Tj + jp) * P.qk_stride + d;
-      *(u32x2*)dst = u32x2{pack_bf16x2(y0, y1), pack_bf16x2(y2, y3)};
-      if (d + 4 == dh && P.qk_stride > dh)  // zero the row's padding (head_dim 72 -> 80)
-        for (int z = 4; z < P.qk_stride - dh + 4; z += 4) *(u32x2*)(dst + z) = u32x2{0u, 0u};
+    for (int q = 0; q < NCG; ++q) {
+      const int n = nw0 + ((lane + 64 * q) % CPR) * 4;  // N is a multiple of 4
+      const u32x2 w = n < N ? *(const u32x2*)(bias + n) : u32x2{0u, 0u};
+      bias4[q] = f32x4{__uint_as_float(w[0] << 16), __uint_as_float(w[0] & 0xFFFF0000u),
+                       __uint_as_float(w[1] << 16), __uint_as_float(w[1] & 0xFFFF0000u)};
+      if (RES)
+        gate4[q] = n < N ? *(const f32x4*)(P.gate + (long)b0 * P.gate_stride + n) : f32x4{0.f, 0.f, 0.f, 0.f};
     }
   }
-}
 
-template <int BM, int BN, int STAGES, int EPI>
-__global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs args) {
-  using C = GemmCfg<BM, BN, STAGES>;
+  // Residual rows of the slab at global row mb (EPI_RESID only).
+  __device__ __forceinline__ void load_resid(f32x4 (&x)[NX], const GemmProb& P, int mb, int nw0, int lane) const {
+    if (!RES) return;
+#pragma unroll
+    for (int it = 0; it < PL; ++it) {
+      const int c = lane + 64 * it;
+      const int m = mb + c / CPR, n = nw0 + (c % CPR) * 4;
+      x[it] = m < P.M && n < P.N ? *(const f32x4*)(P.resid + (long)m * P.N + n) : f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+  }
+
+  __device__ __forceinline__ void apply(const GemmProb& P, const float* Cw, int mb, int nw0, bool vcols, int lane,
+                                        const f32x4 (&x)[NX]) const {
+    const int rpb = P.rows_per_batch, M = P.M, N = P.N;
+    const float inv_rpb = 1.0f / (float)rpb;  // wave-uniform, for div_exact
+    if (EPI == EPI_QKV && vcols) {
+      // v^T[b][h][d][j]: lane takes one column and four consecutive rows.
+      const int D = P.hidden, dh = P.head_dim;
+      const float inv_dh = 1.0f / (float)dh;
+      float cv[PL][4];  // all LDS reads first: one wait for the slab, not one per group
+#pragma unroll
+      for (int it = 0; it < PL; ++it) {
+        const int c = lane + 64 * it;
+        const int col = c >> 3, r4 = (c & 7) * 4;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) cv[it][e] = Cw[(r4 + e) * CST + col];
+      }
+#pragma unroll
+      for (int it = 0; it < PL; ++it) {
+        const int c = lane + 64 * it;
+        const int col = c >> 3, r4 = (c & 7) * 4;
+        const int n = nw0 + col, m = mb + r4;
+        if (n >= N || m >= M) continue;
+        const int rem = n - 2 * D, h = div_exact(rem, dh, inv_dh), d = rem - h * dh;
+        const float bv = vb[it];
+        const int b = div_exact(m, rpb, inv_rpb), jp = m - b * rpb + P.seq_off;
+        const float v0 = cv[it][0] + bv, v1 = cv[it][1] + bv, v2 = cv[it][2] + bv, v3 = cv[it][3] + bv;
+        if (m + 3 < M && jp - P.seq_off + 3 < rpb && (jp & 3) == 0) {
+          bf16_t* vt = (bf16_t*)P.v + (((long)b * P.heads + h) * dh + d) * P.Tj_pad + jp;
+          *(u32x2*)vt = u32x2{pack_bf16x2(v0, v1), pack_bf16x2(v2, v3)};
+        } else {
+          const float vv[4] = {v0, v1, v2, v3};
+          for (int e = 0; e < 4 && m + e < M; ++e) {
+            const int be = div_exact(m + e, rpb, inv_rpb), je = (m + e) - be * rpb + P.seq_off;
+            ((bf16_t*)P.v)[(((long)be * P.heads + h) * dh + d) * P.Tj_pad + je] = f2bf(vv[e]);
+          }
+        }
+      }
+      return;
+    }
+    f32x4 cy[PL];  // all LDS reads first: one wait for the slab, not one per group
+#pragma unroll
+    for (int it = 0; it < PL; ++it) {
+      const int c = lane + 64 * it;
+      cy[it] = *(const f32x4*)&Cw[(c / CPR) * CST + (c % CPR) * 4];
+    }
+#pragma unroll
+    for (int it = 0; it < PL; ++it) {
+      const int c = lane + 64 * it;
+      const int row = c / CPR, c4 = (c % CPR) * 4;
+      const int m = mb + row, n = nw0 + c4;
+      if (m >= M || n >= N) continue;  // N is a multiple of 4
+      const f32x4 y = cy[it];
+      const f32x4 bq = bias4[it % NCG];
+      const float y0 = y[0] + bq[0], y1 = y[1] + bq[1], y2 = y[2] + bq[2], y3 = y[3] + bq[3];
+      if (RES) {
+        const int b = div_exact(m, rpb, inv_rpb);
+        f32x4 g = gate4[it % NCG];
+        if (b != b0) g = *(const f32x4*)(P.gate + (long)b * P.gate_stride + n);  // strip spans two samples
+        f32x4 xv = x[it];
+        xv[0] += g[0] * y0;
+        xv[1] += g[1] * y1;
+        xv[2] += g[2] * y2;
+        xv[3] += g[3] * y3;
+        *(f32x4*)(P.resid + (long)m * N + n) = xv;
+      } else if (EPI == EPI_GELU) {
+        *(u32x2*)((bf16_t*)P.out + (long)m * N + n) =
+            u32x2{pack_bf16x2(gelu_tanh(y0), gelu_tanh(y1)), pack_bf16x2(gelu_tanh(y2), gelu_tanh(y3))};
+      } else if (EPI == EPI_STORE) {
+        *(f32x4*)((float*)P.out + (long)m * N + n) = f32x4{y0, y1, y2, y3};
+      } else {  // EPI_QKV, q and k columns: 4 consecutive d of one head
+        const int D = P.hidden, dh = P.head_dim;
+        const int s = div_exact(n, D, 1.0f / (float)D), rem = n - s * D;
+        const int h = div_exact(rem, dh, 1.0f / (float)dh), d = rem - h * dh;
+        const int b = div_exact(m, rpb, inv_rpb), jp = m - b * rpb + P.seq_off;
+        bf16_t* dst = (bf16_t*)(s == 0 ? P.q : P.k) + (((long)b * P.heads + h) * P.Tj + jp) * P.qk_stride + d;
+        *(u32x2*)dst = u32x2{pack_bf16x2(y0, y1), pack_bf16x2(y2, y3)};
+        if (d + 4 == dh && P.qk_stride > dh)  // zero the row's padding (head_dim 72 -> 80)
+          for (int z = 4; z < P.qk_stride - dh + 4; z += 4) *(u32x2*)(dst + z) = u32x2{0u, 0u};
+      }
+    }
+  }
+};
+
+template <int BM, int BN, int WGM, int WGN, int STAGES, int EPI>
+__global__ __launch_bounds__(WGM * WGN * 64) void gemm_bf16_kernel(GemmArgs args) {
+  using C = GemmCfg<BM, BN, WGM, WGN, STAGES>;
   __shared__ __attribute__((aligned(1024))) unsigned char smem[C::LDS];
 
   const int tile = xcd_remap(blockIdx.x, args.total_tiles);
@@ -167,28 +243,29 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs args) {
   const int KT = K / C::BK;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform (scalar) index
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / WGN, wn = wave - wm * WGN;
   const int r32 = lane & 31, g = lane >> 5;
   const unsigned lds0 = __builtin_amdgcn_readfirstlane(lds_address(smem));
 
-  // DMA instruction t of this wave fills slice rows 8q .. 8q+7, q = wave + 4t;
+  // DMA instruction t of this wave fills slice rows 8q .. 8q+7, q = wave + NW t;
   // lane -> row 8q + lane/8 at stored position lane%8, which holds chunk
-  // (lane%8) ^ f(row) = (lane%8) ^ (lane/8) ^ (q&1), and q&1 = wave&1.
+  // (lane%8) ^ f(row) = (lane%8) ^ (lane/8) ^ (q&1), and q&1 = wave&1 (NW even).
   const int cfetch = (lane & 7) ^ (lane >> 3) ^ (wave & 1);
   unsigned voff[C::IPW];
 #pragma unroll
   for (int t = 0; t < C::IPW; ++t) {
-    const int row = 8 * (wave + 4 * t) + (lane >> 3);
+    const int row = 8 * (wave + C::NW * t) + (lane >> 3);
     const int grow = t < C::IPW_A ? min(m0 + row, M - 1) : min(n0 + row - BM, N - 1);  // clamped: ragged tiles
     voff[t] = (unsigned)grow * (unsigned)K * 2u + (unsigned)cfetch * 16u;
   }
+  // DMA instruction t (0 <= t < IPW) of this wave for a slice into a slot.
+  auto dma_one = [&](int slice, int slot, int t) {
+    const bf16_t* src = (t < C::IPW_A ? A : W) + (long)slice * C::BK;
+    dma_16s(src, voff[t], lds0 + (unsigned)(slot * C::SLICE + wave * 1024 + t * C::NW * 1024));
+  };
   auto issue = [&](int slice, int slot) {
-    const long kb = (long)slice * C::BK;
-    const bf16_t* sa = A + kb;
-    const bf16_t* sw = W + kb;
-    const unsigned base = lds0 + (unsigned)(slot * C::SLICE) + (unsigned)(wave * 1024);
 #pragma unroll
-    for (int t = 0; t < C::IPW; ++t) dma_16s(t < C::IPW_A ? sa : sw, voff[t], base + (unsigned)(t * 4096));
+    for (int t = 0; t < C::IPW; ++t) dma_one(slice, slot, t);
   };
 
   // LDS read offsets of this lane's fragments within a slice buffer, per k-step s.
@@ -224,6 +301,31 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs args) {
   _Pragma("unroll") for (int i = 0; i < C::TM; ++i) _Pragma("unroll") for (int j = 0; j < C::TN; ++j) \
     acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(FA[i], FB[j], acc[i][j], 0, 0, 0);
 #define SCHED_FENCE() __builtin_amdgcn_sched_barrier(0)
+  // One k-step's MFMAs with DMA instructions T0 .. T0+ND-1 of slice DSL
+  // (into slot DSLOT) placed one after each MFMA, so the wave never waits for
+  // the address unit with an MFMA still to issue.
+#define GEMM_MFMA_DMA(FA, FB, ON, DSL, DSLOT, T0, ND)                                         \
+  do {                                                                                       \
+    _Pragma("unroll") for (int q = 0; q < C::TM * C::TN; ++q) {                              \
+      acc[q / C::TN][q % C::TN] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(                   \
+          FA[q / C::TN], FB[q % C::TN], acc[q / C::TN][q % C::TN], 0, 0, 0);                 \
+      if (q < (ND)) {                                                                        \
+        SCHED_FENCE();                                                                       \
+        if (ON) dma_one(DSL, DSLOT, (T0) + q);                                               \
+        SCHED_FENCE();                                                                       \
+      }                                                                                      \
+    }                                                                                        \
+    _Pragma("unroll") for (int q = C::TM * C::TN; q < (ND); ++q) if (ON) dma_one(DSL, DSLOT, (T0) + q); \
+  } while (0)
+
+  // Epilogue constants (bias, gate) are requested first, so they are resident
+  // long before the epilogue; being older than every DMA, they never delay
+  // the explicit vmcnt waits below.
+  using E = Epilogue<EPI, C::WTN, C::CST>;
+  const int nw0 = n0 + wn * C::WTN;
+  const bool vcols = EPI == EPI_QKV && n0 >= 2 * P.hidden;  // tiles never straddle k|v (2D % BN == 0)
+  E epi;
+  epi.init(P, nw0, m0 + wm * C::WTM, vcols, lane);
 
   // Slices past the end are not issued; where fewer than the steady-state
   // number are in flight, the waits fall back to vmcnt(0).
@@ -240,15 +342,21 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs args) {
   // the previous k-step's MFMAs.  After the last reads of slot kt, the wave
   // waits for its DMA of slice kt+1; the workgroup barrier then guarantees
   // every wave's DMA of kt+1 has landed and every read of slot kt is
-  // complete, so slice kt+STAGES is issued into that slot.
+  // complete, so slice kt+STAGES may be written into that slot.  Its DMA
+  // instructions are spread over two MFMA groups (the last k-step of slice kt
+  // and the first of slice kt+1): issued as one burst, the whole workgroup's
+  // DMA queues behind the address unit (16 cycles per 1 KB instruction) and
+  // the waves stall at issue with their MFMAs still to go.
+  constexpr int H1 = C::IPW / 2, H2 = C::IPW - H1;
   bf16x8 xa[C::TM], xb[C::TN], ya[C::TM], yb[C::TN];
   GEMM_READ(xa, xb, 0, 0);
   int slot = 0;
   for (int kt = 0; kt < KT; ++kt) {
     const int next = slot + 1 == STAGES ? 0 : slot + 1;
+    const int prev = slot == 0 ? STAGES - 1 : slot - 1;  // slot of slice kt-1, refilled with kt-1+STAGES
     GEMM_READ(ya, yb, slot, 1);
     SCHED_FENCE();
-    GEMM_MFMA(xa, xb);
+    GEMM_MFMA_DMA(xa, xb, kt >= 1 && kt - 1 + STAGES < KT, kt - 1 + STAGES, prev, H1, H2);
     SCHED_FENCE();
     GEMM_READ(xa, xb, slot, 2);
     SCHED_FENCE();
@@ -261,35 +369,46 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs args) {
     if (kt + STAGES - 1 < KT) wait_vmcnt<(STAGES - 2) * C::IPW>();  // own DMA of slice kt+1 landed
     else wait_vmcnt<0>();
     __syncthreads();
-    if (kt + STAGES < KT) issue(kt + STAGES, slot);
     GEMM_READ(xa, xb, next, 0);  // past the last slice this reads stale data, unused
     SCHED_FENCE();
-    GEMM_MFMA(ya, yb);
+    GEMM_MFMA_DMA(ya, yb, kt + STAGES < KT, kt + STAGES, slot, 0, H1);
     SCHED_FENCE();
     slot = next;
   }
 #undef GEMM_READ
 #undef GEMM_MFMA
+#undef GEMM_MFMA_DMA
 #undef SCHED_FENCE
 
   // ---------------------------------------------------------------- epilogue
-  // Per 32-row slab i: each wave writes its 32 x (BN/2) accumulators to its
-  // own LDS region (column r32 + 32j, rows 8*jj + 4*g + ii), then reads them
-  // back four columns (or, for v^T, four rows) per lane.
+  // Per 32-row slab i: each wave writes its 32 x WTN accumulators to its own
+  // LDS region (column r32 + 32j, rows 8*jj + 4*g + ii), then reads them back
+  // four columns (or, for v^T, four rows) per lane.  The residual rows of
+  // slab i+1 are requested before slab i is processed.
+  // A wave only reads back its own LDS region, and the LDS executes one
+  // wave's instructions in order, so after one workgroup barrier (every wave
+  // is done with the slice ring, which the regions overlap) the slabs need
+  // no further barriers, only a wavefront-scope fence that keeps the
+  // compiler from reordering the lanes' LDS writes and reads.
   float* const Cw = reinterpret_cast<float*>(smem) + wave * 32 * C::CST;
-  const int nw0 = n0 + wn * C::WTN;
-  const bool vcols = EPI == EPI_QKV && n0 >= 2 * P.hidden;  // tiles never straddle k|v (2D % BN == 0)
+  const int mw0 = m0 + wm * C::WTM;
+  f32x4 xcur[E::NX], xnext[E::NX];
+  epi.load_resid(xcur, P, mw0, nw0, lane);
+  __syncthreads();
 #pragma unroll
   for (int i = 0; i < C::TM; ++i) {
-    __syncthreads();
+    wave_lds_fence();
 #pragma unroll
     for (int j = 0; j < C::TN; ++j)
 #pragma unroll
       for (int jj = 0; jj < 4; ++jj)
 #pragma unroll
         for (int ii = 0; ii < 4; ++ii) Cw[(jj * 8 + g * 4 + ii) * C::CST + j * 32 + r32] = acc[i][j][jj * 4 + ii];
-    __syncthreads();
-    epilogue_slab<EPI, C::WTN, C::CST>(P, Cw, m0 + wm * C::WTM + i * 32, nw0, vcols, lane);
+    wave_lds_fence();
+    if (i + 1 < C::TM) epi.load_resid(xnext, P, mw0 + (i + 1) * 32, nw0, lane);
+    epi.apply(P, Cw, mw0 + i * 32, nw0, vcols, lane, xcur);
+#pragma unroll
+    for (int t = 0; t < E::NX; ++t) xcur[t] = xnext[t];
   }
 }
 
@@ -361,17 +480,14 @@ __global__ __launch_bounds__(384) void gemm_bf16_144_kernel(GemmArgs args) {
     const int grow = q < C::BM / 8 ? min(m0 + row, M - 1) : q < C::NDMA ? min(n0 + row - C::BM, N - 1) : 0;
     voff[t] = (unsigned)grow * (unsigned)K * 2u + (unsigned)cfetch * 16u;
   }
+  auto dma_one = [&](int slice, int slot, int t) {
+    const int q = wave + C::NW * t;  // wave-uniform
+    const unsigned dst = q < C::NDMA ? lds0 + (unsigned)(slot * C::SLICE + q * 1024) : lds0 + (unsigned)C::SPARE;
+    dma_16s((q < C::BM / 8 || q >= C::NDMA ? A : W) + (long)slice * C::BK, voff[t], dst);
+  };
   auto issue = [&](int slice, int slot) {
-    const long kb = (long)slice * C::BK;
-    const bf16_t* sa = A + kb;
-    const bf16_t* sw = W + kb;
-    const unsigned base = lds0 + (unsigned)(slot * C::SLICE);
 #pragma unroll
-    for (int t = 0; t < C::IPW; ++t) {
-      const int q = wave + C::NW * t;  // wave-uniform
-      const unsigned dst = q < C::NDMA ? base + (unsigned)(q * 1024) : lds0 + (unsigned)C::SPARE;
-      dma_16s(q < C::BM / 8 || q >= C::NDMA ? sa : sw, voff[t], dst);
-    }
+    for (int t = 0; t < C::IPW; ++t) dma_one(slice, slot, t);
   };
 
   // fragment offsets per 32-wide k-step s (two per slice)
@@ -408,6 +524,27 @@ __global__ __launch_bounds__(384) void gemm_bf16_144_kernel(GemmArgs args) {
   _Pragma("unroll") for (int i = 0; i < C::TM; ++i) _Pragma("unroll") for (int j = 0; j < C::TN; ++j) \
     acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(FA[i], FB[j], acc[i][j], 0, 0, 0);
 #define SCHED_FENCE() __builtin_amdgcn_sched_barrier(0)
+  // As in the kernel above: a slice's DMA instructions are placed between the
+  // MFMAs of two k-steps instead of being issued as one burst.
+#define G144_MFMA_DMA(FA, FB, ON, DSL, DSLOT, T0, ND)                                         \
+  do {                                                                                       \
+    _Pragma("unroll") for (int q = 0; q < C::TM * C::TN; ++q) {                              \
+      acc[q / C::TN][q % C::TN] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(                   \
+          FA[q / C::TN], FB[q % C::TN], acc[q / C::TN][q % C::TN], 0, 0, 0);                 \
+      if (q < (ND)) {                                                                        \
+        SCHED_FENCE();                                                                       \
+        if (ON) dma_one(DSL, DSLOT, (T0) + q);                                               \
+        SCHED_FENCE();                                                                       \
+      }                                                                                      \
+    }                                                                                        \
+    _Pragma("unroll") for (int q = C::TM * C::TN; q < (ND); ++q) if (ON) dma_one(DSL, DSLOT, (T0) + q); \
+  } while (0)
+
+  using E = Epilogue<EPI, C::WTN, C::CST>;
+  const int mw0 = m0 + wm * C::WTM, nw0 = n0 + wn * C::WTN;
+  const bool vcols = EPI == EPI_QKV && n0 >= 2 * P.hidden;  // the host only picks 144 when 2D % 144 == 0
+  E epi;
+  epi.init(P, nw0, mw0, vcols, lane);
 
 #pragma unroll
   for (int s = 0; s < C::STAGES; ++s)
@@ -415,30 +552,34 @@ __global__ __launch_bounds__(384) void gemm_bf16_144_kernel(GemmArgs args) {
   if (KT >= C::STAGES) wait_vmcnt<(C::STAGES - 1) * C::IPW>();
   else wait_vmcnt<0>();
   __syncthreads();
+  constexpr int H1 = C::IPW / 2, H2 = C::IPW - H1;
   G144_READ(xa, xb, 0, 0);
   int slot = 0;
   for (int kt = 0; kt < KT; ++kt) {
     const int next = slot + 1 == C::STAGES ? 0 : slot + 1;
+    const int prev = slot == 0 ? C::STAGES - 1 : slot - 1;  // slot of slice kt-1, refilled with kt-1+STAGES
     G144_READ(ya, yb, slot, 1);
     SCHED_FENCE();
-    G144_MFMA(xa, xb);
+    G144_MFMA_DMA(xa, xb, kt >= 1 && kt - 1 + C::STAGES < KT, kt - 1 + C::STAGES, prev, H1, H2);
     SCHED_FENCE();
     if (kt + C::STAGES - 1 < KT) wait_vmcnt<(C::STAGES - 2) * C::IPW>();  // own DMA of slice kt+1 landed
     else wait_vmcnt<0>();
     __syncthreads();
-    if (kt + C::STAGES < KT) issue(kt + C::STAGES, slot);
     G144_READ(xa, xb, next, 0);  // past the last slice this reads stale data, unused
     SCHED_FENCE();
-    G144_MFMA(ya, yb);
+    G144_MFMA_DMA(ya, yb, kt + C::STAGES < KT, kt + C::STAGES, slot, 0, H1);
     SCHED_FENCE();
     slot = next;
   }
 #undef G144_READ
 #undef G144_MFMA
+#undef G144_MFMA_DMA
 #undef SCHED_FENCE
 
   // epilogue: each wave stages its 32 x 48 accumulators in its own LDS region
   float* const Cw = reinterpret_cast<float*>(smem) + wave * 32 * C::CST;
+  f32x4 xr[E::NX];
+  epi.load_resid(xr, P, mw0, nw0, lane);
   __syncthreads();
 #pragma unroll
   for (int i = 0; i < C::TM; ++i)
@@ -446,14 +587,18 @@ __global__ __launch_bounds__(384) void gemm_bf16_144_kernel(GemmArgs args) {
     for (int j = 0; j < C::TN; ++j)
 #pragma unroll
       for (int e = 0; e < 4; ++e) Cw[(i * 16 + 4 * g4 + e) * C::CST + j * 16 + r16] = acc[i][j][e];
-  __syncthreads();
-  const bool vcols = EPI == EPI_QKV && n0 >= 2 * P.hidden;  // the host only picks 144 when 2D % 144 == 0
-  epilogue_slab<EPI, C::WTN, C::CST>(P, Cw, m0 + wm * C::WTM, n0 + wn * C::WTN, vcols, lane);
+  wave_lds_fence();  // own region only: the LDS runs a wave's accesses in order
+  epi.apply(P, Cw, mw0, nw0, vcols, lane, xr);
 }
 
 void gemm_tile_dims(int tile_cfg, int* bm, int* bn) {
-  *bm = tile_cfg == TILE_128x128 ? 128 : 64;
-  *bn = tile_cfg == TILE_64x144 ? 144 : 128;
+  switch (tile_cfg) {
+    case TILE_128x128: *bm = 128; *bn = 128; break;
+    case TILE_64x144: *bm = 64; *bn = 144; break;
+    case TILE_256x256: *bm = 256; *bn = 256; break;
+    case TILE_256x128: *bm = 256; *bn = 128; break;
+    default: *bm = 64; *bn = 128; break;
+  }
 }
 
 static hipError_t launch_144(const GemmArgs& a, int epi, hipStream_t st) {
@@ -468,28 +613,35 @@ static hipError_t launch_144(const GemmArgs& a, int epi, hipStream_t st) {
   return hipGetLastError();
 }
 
-template <int BM, int BN, int STAGES>
+template <int BM, int BN, int WGM, int WGN, int STAGES>
 static hipError_t launch_tile(const GemmArgs& a, int epi, hipStream_t st) {
-  dim3 grid(a.total_tiles), block(256);
+  dim3 grid(a.total_tiles), block(WGM * WGN * 64);
+#define GEMM_EPI_CASE(E) hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, WGM, WGN, STAGES, E>), grid, block, 0, st, a)
   switch (epi) {
-    case EPI_QKV: hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, STAGES, EPI_QKV>), grid, block, 0, st, a); break;
-    case EPI_GELU: hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, STAGES, EPI_GELU>), grid, block, 0, st, a); break;
-    case EPI_RESID: hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, STAGES, EPI_RESID>), grid, block, 0, st, a); break;
-    case EPI_RESID2: hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, STAGES, EPI_RESID2>), grid, block, 0, st, a); break;
-    default: hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, STAGES, EPI_STORE>), grid, block, 0, st, a); break;
+    case EPI_QKV: GEMM_EPI_CASE(EPI_QKV); break;
+    case EPI_GELU: GEMM_EPI_CASE(EPI_GELU); break;
+    case EPI_RESID: GEMM_EPI_CASE(EPI_RESID); break;
+    case EPI_RESID2: GEMM_EPI_CASE(EPI_RESID2); break;
+    default: GEMM_EPI_CASE(EPI_STORE); break;
   }
+#undef GEMM_EPI_CASE
   return hipGetLastError();
 }
 
 // Ring depth: a slice is (BM + BN) x 128 bytes, so 128x128 with 2 slots and
 // 64x128 with 3 fit two workgroups per CU (64 KB, 72 KB), and 64x128 with 2
 // slots fits three (48 KB); measured faster than deeper rings with one
-// workgroup per CU.
+// workgroup per CU.  256x256 (2 slots, 128 KB) and 256x128 (3 slots, 144 KB)
+// run one eight-wave workgroup per CU.
 hipError_t launch_gemm_bf16(const GemmArgs& a, int epi, int tile_cfg, hipStream_t st) {
-  if (tile_cfg == TILE_64x128) return launch_tile<64, 128, 3>(a, epi, st);
-  if (tile_cfg == TILE_64x128_S2) return launch_tile<64, 128, 2>(a, epi, st);
-  if (tile_cfg == TILE_64x144) return launch_144(a, epi, st);
-  return launch_tile<128, 128, 2>(a, epi, st);
+  switch (tile_cfg) {
+    case TILE_64x128: return launch_tile<64, 128, 2, 2, 3>(a, epi, st);
+    case TILE_64x128_S2: return launch_tile<64, 128, 2, 2, 2>(a, epi, st);
+    case TILE_64x144: return launch_144(a, epi, st);
+    case TILE_256x256: return launch_tile<256, 256, 2, 4, 2>(a, epi, st);
+    case TILE_256x128: return launch_tile<256, 128, 4, 2, 3>(a, epi, st);
+    default: return launch_tile<128, 128, 2, 2, 2>(a, epi, st);
+  }
 }
 
 }  // namespace ditmi

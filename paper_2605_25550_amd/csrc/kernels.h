@@ -115,7 +115,10 @@ hipError_t launch_fill_f32(float* p, int n, float v, hipStream_t st);
 hipError_t launch_axpy_f32(float* z, const float* v, float a, long n, hipStream_t st);
 
 // Tile configurations of the bf16 GEMM (BM x BN, LDS ring depth).
-enum { TILE_128x128 = 0, TILE_64x128 = 1, TILE_64x128_S2 = 2, TILE_64x144 = 3, TILE_COUNT = 4 };
+enum {
+  TILE_128x128 = 0, TILE_64x128 = 1, TILE_64x128_S2 = 2, TILE_64x144 = 3,
+  TILE_256x256 = 4, TILE_256x128 = 5, TILE_COUNT = 6
+};
 void gemm_tile_dims(int tile_cfg, int* bm, int* bn);
 
 }  // namespace ditmi

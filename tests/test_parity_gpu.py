@@ -75,6 +75,11 @@ SMALL = [
                                                           head_dim=128, mlp_hidden=1024, n_blocks=1)),
     ("bf16_joint_dh72_tt5", synth.CONFIGS["c3"].with_(batch=1, tokens=64, text_tokens=5, hidden=576, heads=8,
                                                       head_dim=72, mlp_hidden=256, n_blocks=1)),
+    # DiT-XL widths with ragged row counts that select the 256-row GEMM tiles:
+    # 2000 rows -> QKV 256x128, fc1 256x256, out/fc2 64x144 (last M tile ragged)
+    ("bf16_xl_t250_b8_tiles", synth.CONFIGS["c1"].with_(batch=8, tokens=250, n_blocks=1)),
+    # 2340 rows -> QKV (incl. the v^T columns) and fc1 on 256x256 tiles
+    ("bf16_xl_t260_b9_tiles", synth.CONFIGS["c1"].with_(batch=9, tokens=260, n_blocks=1)),
 ]
 
 
