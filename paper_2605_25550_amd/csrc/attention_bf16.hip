@@ -11,8 +11,9 @@
 // until the end.  The probabilities are then already laid out as the B
 // operand of O^T = V^T P^T (keys permuted consistently on both operands), and
 // O^T's accumulators again belong to the lane's own query.  V is consumed
-// transposed (v^T [dh][T], written that way by the QKV GEMM epilogue), so its
-// A operand is two 8-byte LDS reads per lane.
+// transposed (v^T [dh][T], written that way by the QKV GEMM epilogue, with the
+// keys of every 16-key group stored in the order of that permutation,
+// kernels.h v_key_pos), so its A operand is one 16-byte LDS read per lane.
 //
 // Schedule.  A workgroup is 8 waves (256 queries; 4 waves for small grids),
 // two waves per SIMD, so one wave's softmax VALU work runs while the other's
@@ -61,7 +62,7 @@ struct AttnCfg {
 };
 
 template <int DH, int NW, int QT>
-__global__ __launch_bounds__(NW * 64, 8 / NW) void attn_bf16_dma_kernel(AttnArgs a) {
+__global__ __launch_bounds__(NW * 64, QT == 1 ? 8 / NW : 1) void attn_bf16_dma_kernel(AttnArgs a) {
   using C = AttnCfg<DH>;
   constexpr int IPW = (C::TDMA + NW - 1) / NW;  // DMA instructions per wave per tile (uniform)
   // ring of slots, then a 1 KB line that absorbs the spare DMAs
@@ -132,12 +133,11 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_bf16_dma_kernel(AttnArgs
   int k_off[C::KS];
 #pragma unroll
   for (int s = 0; s < C::KS; ++s) k_off[s] = r32 * C::KROW + (((2 * s + g) ^ C::swz_k(r32)) << 4);
-  int v_lo[4], v_hi[4];
+  // keys 16c+4g+0..3 and 16c+8+4g+0..3 form logical chunk 2c+g of a V^T row
+  // (v_key_pos order), so each PV operand is one 16-byte read
+  int v_off[4];
 #pragma unroll
-  for (int c = 0; c < 4; ++c) {  // keys 16c+4g.. in logical chunk 2c, keys 16c+8+4g.. in chunk 2c+1
-    v_lo[c] = C::KTILE + r32 * 128 + (((2 * c) ^ C::swz_v(r32)) << 4) + g * 8;
-    v_hi[c] = C::KTILE + r32 * 128 + (((2 * c + 1) ^ C::swz_v(r32)) << 4) + g * 8;
-  }
+  for (int c = 0; c < 4; ++c) v_off[c] = C::KTILE + r32 * 128 + (((2 * c + g) ^ C::swz_v(r32)) << 4);
 
   const float sc = a.scale_log2;
   // Lazy max: probabilities are exp2(s*scale - m_run) <= 2^TAU; bf16 and fp32
@@ -171,7 +171,8 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_bf16_dma_kernel(AttnArgs
       for (int e = tid; e < DH * C::BKV; e += NW * 64) {
         const int d = e / C::BKV, key = e % C::BKV;
         if (key >= nvalid) {
-          const int off = C::KTILE + d * 128 + (((key >> 3) ^ C::swz_v(d)) << 4) + (key & 7) * 2;
+          const int kp = v_key_pos(key);
+          const int off = C::KTILE + d * 128 + (((kp >> 3) ^ C::swz_v(d)) << 4) + (kp & 7) * 2;
           *(bf16_t*)(smem + (it % C::STAGES) * C::SLOT + off) = 0;
         }
       }
@@ -251,9 +252,7 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_bf16_dma_kernel(AttnArgs
       for (int c = 0; c < 4; ++c)
 #pragma unroll
         for (int t = 0; t < C::DT; ++t) {
-          const u32x2 lo = *(const u32x2*)(slot + t * 32 * 128 + v_lo[c]);
-          const u32x2 hi = *(const u32x2*)(slot + t * 32 * 128 + v_hi[c]);
-          const u32x4 vw = {lo[0], lo[1], hi[0], hi[1]};
+          const u32x4 vw = *(const u32x4*)(slot + t * 32 * 128 + v_off[c]);
           oacc[qt][t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, vw),
                                                                  __builtin_bit_cast(bf16x8, pw[qt][c]), oacc[qt][t], 0, 0, 0);
         }
@@ -283,14 +282,286 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_bf16_dma_kernel(AttnArgs
   }
 }
 
+// Software-pipelined variant (one 32-query tile per wave).  Within a wave,
+// the QK^T MFMAs of key tile j+1 are issued between the softmax instructions
+// of tile j, and the PV MFMAs of tile j between the row-max instructions of
+// tile j+1, so the matrix pipe and the VALU work at the same time even while
+// the workgroup barrier keeps the two waves of a SIMD in step.  K of tile
+// j+1 is read one iteration earlier than V of tile j, so the ring has four
+// slots (tile t in slot t % 4, refilled with t + 4 after the barrier that
+// ends iteration t), which keeps two iterations between a tile's DMA and its
+// first read.
+template <int DH, int NW>
+__global__ __launch_bounds__(NW * 64, 1) void attn_bf16_pipe_kernel(AttnArgs a) {
+  using C = AttnCfg<DH>;
+  constexpr int ST = 4;
+  constexpr int IPW = (C::TDMA + NW - 1) / NW;  // DMA instructions per wave per tile (uniform)
+  __shared__ __attribute__((aligned(1024))) unsigned char smem[ST * C::SLOT + 1024];
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int g = lane >> 5, r32 = lane & 31;
+  const int b = blockIdx.z, h = blockIdx.y;
+  const int Tj = a.Tj, Tjp = a.Tj_pad;
+  const long bh = (long)b * a.H + h;
+  const bf16_t* __restrict__ qp = (const bf16_t*)a.q + bh * Tj * C::DHP;
+  const bf16_t* __restrict__ kp = (const bf16_t*)a.k + bh * Tj * C::DHP;
+  const bf16_t* __restrict__ vp = (const bf16_t*)a.v + bh * DH * (long)Tjp;
+  const unsigned lds0 = __builtin_amdgcn_readfirstlane(lds_address(smem));
+  const int q0 = blockIdx.x * (NW * 32) + wave * 32;  // first query of this wave
+  const int nkv = (Tj + C::BKV - 1) / C::BKV;
+
+  // DMA of one tile (layout as in the kernel above) into slot tile % ST.  The
+  // sources are a scalar base (the tile's first K row / V^T column) plus a
+  // 32-bit lane offset, fixed for every full tile; only a tile reaching past
+  // Tj clamps (K rows past the end re-read row Tj-1, V^T chunks past Tj_pad
+  // re-read the last chunk).  Spare instructions re-read instruction 0's K
+  // rows into a scratch line, keeping the per-wave DMA count uniform.
+  auto dma_off = [&](int t, int rmax, int cmax) -> unsigned {
+    const int qi = (t < 0 ? 0 : t) * NW + wave, byte = qi * 1024 + lane * 16;
+    if (qi < C::KDMA || t < 0) {
+      const int R = byte / C::KROW, pos = (byte % C::KROW) >> 4;
+      return (unsigned)(min(R, rmax) * (C::DHP * 2) + (pos ^ C::swz_k(R)) * 16);
+    }
+    const int vb = byte - C::KTILE, d = vb >> 7, pos = (vb & 127) >> 4;
+    return (unsigned)((d * Tjp + min((pos ^ C::swz_v(d)) * 8, cmax)) * 2);
+  };
+  unsigned doff[IPW];
+#pragma unroll
+  for (int t = 0; t < IPW; ++t) doff[t] = dma_off(wave + NW * t < C::TDMA ? t : -1, C::BKV, C::BKV);
+  auto issue = [&](int tile) {
+    const int kv0 = tile * C::BKV;
+    const unsigned base = lds0 + (unsigned)((tile % ST) * C::SLOT);
+    const bf16_t* kb = kp + (long)kv0 * C::DHP;  // wave-uniform
+    const bf16_t* vb = vp + kv0;
+    const bool full = kv0 + C::BKV <= Tj;
+#pragma unroll
+    for (int t = 0; t < IPW; ++t) {
+      const int qi = wave + NW * t;  // wave-uniform
+      const bool kpart = qi < C::KDMA || qi >= C::TDMA;
+      const unsigned off = full ? doff[t] : dma_off(qi < C::TDMA ? t : -1, Tj - 1 - kv0, Tjp - 8 - kv0);
+      const unsigned dst = qi < C::TDMA ? base + (unsigned)(qi * 1024) : lds0 + (unsigned)(ST * C::SLOT);
+      dma_16s(kpart ? (const void*)kb : (const void*)vb, off, dst);
+    }
+  };
+  // V^T columns of keys past the end (last tile only) hold stale workspace
+  // bytes; zero them so that their zero probabilities cannot meet a NaN.
+  auto zero_v_tail = [&](int tile) {
+    const int kv0 = tile * C::BKV, nvalid = Tj - kv0;
+    unsigned char* sl = smem + (tile % ST) * C::SLOT;
+    for (int e = tid; e < DH * C::BKV; e += NW * 64) {
+      const int d = e / C::BKV, key = e % C::BKV;
+      const int kp = v_key_pos(key);
+      if (key >= nvalid) *(bf16_t*)(sl + C::KTILE + d * 128 + (((kp >> 3) ^ C::swz_v(d)) << 4) + (kp & 7) * 2) = 0;
+    }
+  };
+
+  // V^T rows past head_dim (head_dim 72 only) are never written by the DMA.
+  if (C::VROWS > DH) {
+    for (int e = tid; e < ST * (C::VROWS - DH) * 32; e += NW * 64) {
+      const int sl = e / ((C::VROWS - DH) * 32), w = e % ((C::VROWS - DH) * 32);
+      ((uint32_t*)(smem + sl * C::SLOT + C::KTILE + DH * 128))[w] = 0u;
+    }
+  }
+
+  bf16x8 qf[C::KS];
+  {
+    const int qrow = q0 + r32;
+#pragma unroll
+    for (int s = 0; s < C::KS; ++s)
+      qf[s] = qrow < Tj ? *(const bf16x8*)(qp + (long)qrow * C::DHP + s * 16 + g * 8) : bf16x8{};
+  }
+  int k_off[C::KS];
+#pragma unroll
+  for (int s = 0; s < C::KS; ++s) k_off[s] = r32 * C::KROW + (((2 * s + g) ^ C::swz_k(r32)) << 4);
+  int v_off[4];
+#pragma unroll
+  for (int c = 0; c < 4; ++c) v_off[c] = C::KTILE + r32 * 128 + (((2 * c + g) ^ C::swz_v(r32)) << 4);
+
+  const float sc = a.scale_log2;
+  const float TAU = 64.0f;  // lazy max, as in the kernel above
+  float m_run = -INFINITY, l_run = 0.f;
+  f32x16 oacc[C::DT];
+#pragma unroll
+  for (int t = 0; t < C::DT; ++t) oacc[t] = f32x16{};
+
+  // S^T of one key tile: accumulators start at -inf for keys past the end.
+  auto qk = [&](int tile, f32x16 (&s)[2]) {
+    const int kv0 = tile * C::BKV;
+    const unsigned char* sl = smem + (tile % ST) * C::SLOT;
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt) {
+      f32x16 init = f32x16{};
+      if (kv0 + C::BKV > Tj) {
+#pragma unroll
+        for (int e = 0; e < 16; ++e)
+          init[e] = kv0 + kt * 32 + (e >> 2) * 8 + g * 4 + (e & 3) < Tj ? 0.f : -INFINITY;
+      }
+      s[kt] = init;
+    }
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+      for (int st = 0; st < C::KS; ++st) {
+        const bf16x8 kf = *(const bf16x8*)(sl + kt * 32 * C::KROW + k_off[st]);
+        s[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[st], s[kt], 0, 0, 0);
+      }
+  };
+  auto rowmax = [&](const f32x16 (&s)[2]) {
+    float m = -INFINITY;
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) m = fmaxf(m, s[kt][e]);
+    return max_halves(m) * sc;
+  };
+
+  // prologue: tiles 0..3 in flight; tiles 0 and 1 landed before the loop
+#pragma unroll
+  for (int t = 0; t < ST; ++t)
+    if (t < nkv) issue(t);
+  if (nkv >= 4) wait_vmcnt<2 * IPW>();
+  else if (nkv == 3) wait_vmcnt<IPW>();
+  else wait_vmcnt<0>();
+  __syncthreads();
+  if (nkv <= 2) {  // the last tile has landed already (else: zeroed at the end of iteration nkv-3)
+    zero_v_tail(nkv - 1);
+    __syncthreads();
+  }
+  f32x16 scur[2], snext[2];
+  qk(0, scur);
+  float mcur = rowmax(scur);
+
+  for (int j = 0; j < nkv; ++j) {
+    // lazy rescale for tile j
+    if (m_run == -INFINITY) {
+      m_run = mcur;
+    } else if (__builtin_amdgcn_ballot_w64(mcur > m_run + TAU) != 0) {
+      const float m_new = fmaxf(m_run, mcur);
+      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+      l_run *= alpha;
+#pragma unroll
+      for (int t = 0; t < C::DT; ++t) oacc[t] *= alpha;
+      m_run = m_new;
+    }
+    // Softmax of tile j interleaved by hand with the QK^T MFMAs of tile j+1
+    // (unconditional: the last iteration recomputes the last tile, unused):
+    // K fragments are read two MFMAs ahead, the MFMAs alternate between the
+    // two 32-key halves (independent accumulators), and each MFMA is
+    // followed by its share of the exponentials.
+    {
+      const int tn = min(j + 1, nkv - 1), kvn = tn * C::BKV;
+      const unsigned char* sln = smem + (tn % ST) * C::SLOT;
+#pragma unroll
+      for (int kt = 0; kt < 2; ++kt) {
+        f32x16 init = f32x16{};
+        if (kvn + C::BKV > Tj) {
+#pragma unroll
+          for (int e = 0; e < 16; ++e)
+            init[e] = kvn + kt * 32 + (e >> 2) * 8 + g * 4 + (e & 3) < Tj ? 0.f : -INFINITY;
+        }
+        snext[kt] = init;
+      }
+      constexpr int NQ = 2 * C::KS;  // QK^T MFMAs per tile; MFMA i: half i % 2, k-step i / 2
+      auto kread = [&](int i) { return *(const bf16x8*)(sln + (i & 1) * 32 * C::KROW + k_off[i >> 1]); };
+      bf16x8 kf[3];
+      kf[0] = kread(0);
+      kf[1] = kread(1);
+      const float mneg = -m_run;
+      float lsum = 0.f;
+#pragma unroll
+      for (int i = 0; i < NQ; ++i) {
+        if (i + 2 < NQ) kf[(i + 2) % 3] = kread(i + 2);
+        snext[i & 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[i % 3], qf[i >> 1], snext[i & 1], 0, 0, 0);
+#pragma unroll
+        for (int e = i * 32 / NQ; e < (i + 1) * 32 / NQ; ++e) {
+          const float p = __builtin_amdgcn_exp2f(fmaf(scur[e >> 4][e & 15], sc, mneg));
+          scur[e >> 4][e & 15] = p;
+          lsum += p;
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      l_run += lsum;
+    }
+    u32x4 pw[4];
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const int kt = c >> 1, jb = (c & 1) * 2;
+      pw[c] = u32x4{pack_bf16x2(scur[kt][jb * 4 + 0], scur[kt][jb * 4 + 1]),
+                    pack_bf16x2(scur[kt][jb * 4 + 2], scur[kt][jb * 4 + 3]),
+                    pack_bf16x2(scur[kt][jb * 4 + 4], scur[kt][jb * 4 + 5]),
+                    pack_bf16x2(scur[kt][jb * 4 + 6], scur[kt][jb * 4 + 7])};
+    }
+    // PV of tile j (consecutive MFMAs on different O^T tiles), V^T read two
+    // MFMAs ahead, interleaved with the row max of tile j+1.
+    {
+      const unsigned char* sl = smem + (j % ST) * C::SLOT;
+      constexpr int NP = 4 * C::DT;  // MFMA i: key chunk i / DT, O^T tile i % DT
+      auto vread = [&](int i) {
+        const int c = i / C::DT, t = i % C::DT;
+        return *(const u32x4*)(sl + t * 32 * 128 + v_off[c]);
+      };
+      u32x4 vf[3];
+      vf[0] = vread(0);
+      vf[1] = vread(1);
+      float m = -INFINITY;
+#pragma unroll
+      for (int i = 0; i < NP; ++i) {
+        if (i + 2 < NP) vf[(i + 2) % 3] = vread(i + 2);
+        oacc[i % C::DT] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, vf[i % 3]),
+                                                                  __builtin_bit_cast(bf16x8, pw[i / C::DT]),
+                                                                  oacc[i % C::DT], 0, 0, 0);
+#pragma unroll
+        for (int e = i * 32 / NP; e < (i + 1) * 32 / NP; ++e) m = fmaxf(m, snext[e >> 4][e & 15]);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      mcur = max_halves(m) * sc;
+    }
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt) scur[kt] = snext[kt];
+    // tile j+2 must have landed for every wave before the next iteration's
+    // QK^T; every wave is done with slot j % ST, which takes tile j+4
+    if (j + 3 < nkv) wait_vmcnt<IPW>();
+    else wait_vmcnt<0>();
+    __syncthreads();
+    if (j + 4 < nkv) issue(j + 4);
+    if (j + 2 == nkv - 1) {  // the last tile's V^T is read in iteration nkv-1
+      zero_v_tail(nkv - 1);
+      __syncthreads();
+    }
+  }
+  wait_vmcnt<0>();
+
+  {
+    const int qrow = q0 + r32;
+    const float inv = 1.0f / sum_halves(l_run);
+    if (qrow < Tj) {
+      const long orow = qrow < a.T_img ? (long)b * a.T_img + qrow
+                                       : (long)a.B * a.T_img + (long)b * a.T_txt + (qrow - a.T_img);
+      bf16_t* op = (bf16_t*)a.o + orow * a.D + h * DH;
+#pragma unroll
+      for (int t = 0; t < C::DT; ++t)
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) {
+          const int d = t * 32 + jj * 8 + g * 4;
+          if (d < DH)
+            *(u32x2*)(op + d) = u32x2{pack_bf16x2(oacc[t][jj * 4 + 0] * inv, oacc[t][jj * 4 + 1] * inv),
+                                      pack_bf16x2(oacc[t][jj * 4 + 2] * inv, oacc[t][jj * 4 + 3] * inv)};
+        }
+    }
+  }
+}
+
 hipError_t launch_attn_bf16(const AttnArgs& a, int head_dim, hipStream_t st) {
-  // 8 waves x 32 queries per workgroup (two waves per SIMD); 4 waves when the
-  // grid would otherwise leave CUs idle.
+  // Enough work items for every CU: the pipelined kernel, 8 waves x 32
+  // queries per workgroup.  Otherwise (few, short sequences) the first
+  // kernel with 4 waves x 32 queries, which spreads the work over twice as
+  // many workgroups.
   const bool wide = (long)((a.Tj + 255) / 256) * a.H * a.B >= 256;
   const int nw = wide ? 8 : 4;
   dim3 grid((a.Tj + nw * 32 - 1) / (nw * 32), a.H, a.B), block(nw * 64);
-#define ATTN_LAUNCH(DHV)                                                                       \
-  if (wide) hipLaunchKernelGGL((attn_bf16_dma_kernel<DHV, 8, 1>), grid, block, 0, st, a);     \
+#define ATTN_LAUNCH(DHV)                                                                   \
+  if (wide) hipLaunchKernelGGL((attn_bf16_pipe_kernel<DHV, 8>), grid, block, 0, st, a);   \
   else hipLaunchKernelGGL((attn_bf16_dma_kernel<DHV, 4, 1>), grid, block, 0, st, a);
   switch (head_dim) {
     case 64: ATTN_LAUNCH(64) break;

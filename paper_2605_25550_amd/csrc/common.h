@@ -124,6 +124,15 @@ __device__ __forceinline__ void dma_16(const void* gsrc, unsigned lds_base) {
                : "memory", "m0");
 }
 
+// 16 bytes per lane from sbase + voff (sbase wave-uniform) into LDS at
+// (wave-uniform) lds_base + 16 * lane.
+__device__ __forceinline__ void dma_16s(const void* sbase, unsigned voff, unsigned lds_base) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2"
+               :
+               : "s"(lds_base), "v"(voff), "s"(sbase)
+               : "memory", "m0");
+}
+
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
   static_assert(N >= 0 && N < 64, "vmcnt range");

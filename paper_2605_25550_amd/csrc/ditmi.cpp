@@ -85,7 +85,7 @@ Layout layout(const dit_shape* s, int kind) {
   const size_t H = s->heads, dh = s->head_dim;
   L.ns = Tt > 0 ? 2 : 1;
   L.Tj = (int)(T + Tt);
-  L.Tj_pad = (int)rup(L.Tj, 8);
+  L.Tj_pad = (int)rup(L.Tj, 16);  // v^T rows: whole 16-key groups (kernels.h: v_key_pos)
   size_t off = 0;
   auto take = [&](size_t bytes) {
     size_t o = off;

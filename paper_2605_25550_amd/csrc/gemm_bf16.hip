@@ -64,15 +64,6 @@ __device__ __forceinline__ void wave_lds_fence() { __builtin_amdgcn_fence(__ATOM
 // Stored position of 16-byte chunk c of slice row r.
 __device__ __forceinline__ int chunk_pos(int r, int c) { return c ^ ((r & 7) ^ ((r >> 3) & 1)); }
 
-// 16 bytes per lane from sbase + voff (sbase wave-uniform) into LDS at
-// (wave-uniform) lds_base + 16 * lane.
-__device__ __forceinline__ void dma_16s(const void* sbase, unsigned voff, unsigned lds_base) {
-  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2"
-               :
-               : "s"(lds_base), "v"(voff), "s"(sbase)
-               : "memory", "m0");
-}
-
 // Fused epilogue of one wave's strip of WTN columns, applied one 32-row slab
 // at a time from fp32 accumulators staged in LDS (row stride CST).  Each lane
 // takes four consecutive columns of one row (or, for the v part of the QKV
@@ -160,14 +151,14 @@ struct Epilogue {
         const float bv = vb[it];
         const int b = div_exact(m, rpb, inv_rpb), jp = m - b * rpb + P.seq_off;
         const float v0 = cv[it][0] + bv, v1 = cv[it][1] + bv, v2 = cv[it][2] + bv, v3 = cv[it][3] + bv;
-        if (m + 3 < M && jp - P.seq_off + 3 < rpb && (jp & 3) == 0) {
-          bf16_t* vt = (bf16_t*)P.v + (((long)b * P.heads + h) * dh + d) * P.Tj_pad + jp;
+        if (m + 3 < M && jp - P.seq_off + 3 < rpb && (jp & 3) == 0) {  // 4 keys stay contiguous under v_key_pos
+          bf16_t* vt = (bf16_t*)P.v + (((long)b * P.heads + h) * dh + d) * P.Tj_pad + v_key_pos(jp);
           *(u32x2*)vt = u32x2{pack_bf16x2(v0, v1), pack_bf16x2(v2, v3)};
         } else {
           const float vv[4] = {v0, v1, v2, v3};
           for (int e = 0; e < 4 && m + e < M; ++e) {
             const int be = div_exact(m + e, rpb, inv_rpb), je = (m + e) - be * rpb + P.seq_off;
-            ((bf16_t*)P.v)[(((long)be * P.heads + h) * dh + d) * P.Tj_pad + je] = f2bf(vv[e]);
+            ((bf16_t*)P.v)[(((long)be * P.heads + h) * dh + d) * P.Tj_pad + v_key_pos(je)] = f2bf(vv[e]);
           }
         }
       }

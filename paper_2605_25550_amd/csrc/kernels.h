@@ -33,7 +33,7 @@ struct GemmProb {
   // EPI_QKV: row m -> (b, j = m % rows_per_batch + seq_off) of the joint sequence
   void* q;             // [B, H, Tj, qk_stride]
   void* k;             // [B, H, Tj, qk_stride]
-  void* v;             // bf16: v^T [B, H, dh, Tj_pad]; fp32: [B, H, Tj, dh]
+  void* v;             // bf16: v^T [B, H, dh, Tj_pad], key j at column v_key_pos(j); fp32: [B, H, Tj, dh]
   int seq_off, Tj, Tj_pad, heads, head_dim, hidden;
   int qk_stride;       // q/k row length: head_dim, or (bf16) head_dim rounded up to 16, zero padded
 };
@@ -44,11 +44,18 @@ struct GemmArgs {
   int total_tiles;
 };
 
+// Column of key j in a bf16 v^T row: within each group of 16 keys the
+// order is [0..3, 8..11, 4..7, 12..15] (bits 2 and 3 of j swapped), so the
+// eight keys one lane of the attention PV MFMA needs (16c + 4g + 0..3 and
+// 16c + 8 + 4g + 0..3) are one contiguous 16-byte chunk.  Tj_pad is a
+// multiple of 16.
+__host__ __device__ __forceinline__ int v_key_pos(int j) { return (j & ~12) | ((j & 4) << 1) | ((j & 8) >> 1); }
+
 // ------------------------------------------------------------------ attention
 struct AttnArgs {
   const void* q;   // bf16: [B, H, Tj, round16(dh)] zero padded; fp32: [B, H, Tj, dh]
   const void* k;   // same layout as q
-  const void* v;   // bf16: v^T [B, H, dh, Tj_pad]; fp32: [B, H, Tj, dh]
+  const void* v;   // bf16: v^T [B, H, dh, Tj_pad] (key j at column v_key_pos(j)); fp32: [B, H, Tj, dh]
   void* o;         // stream-major rows: image b*T + t, then text B*T + b*Tt + t; [*, H*dh]
   int B, H, Tj, Tj_pad, T_img, T_txt, D;
   float scale_log2;  // log2(e) / sqrt(dh)

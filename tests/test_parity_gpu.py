@@ -80,6 +80,15 @@ SMALL = [
     ("bf16_xl_t250_b8_tiles", synth.CONFIGS["c1"].with_(batch=8, tokens=250, n_blocks=1)),
     # 2340 rows -> QKV (incl. the v^T columns) and fc1 on 256x256 tiles
     ("bf16_xl_t260_b9_tiles", synth.CONFIGS["c1"].with_(batch=9, tokens=260, n_blocks=1)),
+    # >= 256 (sample, head, 256-query) items select the software-pipelined
+    # attention kernel: one, two and three key tiles, ragged last tiles
+    ("bf16_pipe_dh64_t17_b16", synth.CONFIGS["c1"].with_(batch=16, tokens=17, hidden=1024, heads=16, head_dim=64,
+                                                         mlp_hidden=512, n_blocks=1)),
+    ("bf16_pipe_dh128_t100_b32", synth.CONFIGS["c1"].with_(batch=32, tokens=100, hidden=1024, heads=8, head_dim=128,
+                                                           mlp_hidden=512, n_blocks=1)),
+    ("bf16_pipe_dh72_t150_b16", synth.CONFIGS["c1"].with_(batch=16, tokens=150, n_blocks=1)),
+    ("bf16_pipe_joint_dh128", synth.CONFIGS["c3"].with_(batch=32, tokens=120, text_tokens=9, hidden=1024, heads=8,
+                                                        head_dim=128, mlp_hidden=512, n_blocks=1)),
 ]
 
 
