@@ -378,27 +378,36 @@ __global__ __launch_bounds__(NW * 64, 1) void attn_bf16_pipe_kernel(AttnArgs a) 
 #pragma unroll
   for (int c = 0; c < 4; ++c) v_off[c] = C::KTILE + r32 * 128 + (((2 * c + g) ^ C::swz_v(r32)) << 4);
 
-  const float sc = a.scale_log2;
+  // k arrives in the exp2 domain (stored pre-scaled by the QKV epilogue), and
+  // every S^T accumulator starts at -m_run (the running max at the time its
+  // QK^T is issued), so the MFMA result is directly the exp2 argument.
   const float TAU = 64.0f;  // lazy max, as in the kernel above
-  float m_run = -INFINITY, l_run = 0.f;
+  float m_run = 0.f, l_run = 0.f;
+  bool first = true;
   f32x16 oacc[C::DT];
 #pragma unroll
   for (int t = 0; t < C::DT; ++t) oacc[t] = f32x16{};
 
-  // S^T of one key tile: accumulators start at -inf for keys past the end.
-  auto qk = [&](int tile, f32x16 (&s)[2]) {
-    const int kv0 = tile * C::BKV;
-    const unsigned char* sl = smem + (tile % ST) * C::SLOT;
+  // S^T of one key tile minus m_run: accumulators start at -m_run, and at
+  // -inf for keys past the end.
+  auto s_init = [&](int kv0, f32x16 (&s)[2]) {
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt) {
-      f32x16 init = f32x16{};
+      f32x16 init;
+#pragma unroll
+      for (int e = 0; e < 16; ++e) init[e] = -m_run;
       if (kv0 + C::BKV > Tj) {
 #pragma unroll
         for (int e = 0; e < 16; ++e)
-          init[e] = kv0 + kt * 32 + (e >> 2) * 8 + g * 4 + (e & 3) < Tj ? 0.f : -INFINITY;
+          if (kv0 + kt * 32 + (e >> 2) * 8 + g * 4 + (e & 3) >= Tj) init[e] = -INFINITY;
       }
       s[kt] = init;
     }
+  };
+  auto qk = [&](int tile, f32x16 (&s)[2]) {
+    const int kv0 = tile * C::BKV;
+    const unsigned char* sl = smem + (tile % ST) * C::SLOT;
+    s_init(kv0, s);
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
@@ -413,7 +422,7 @@ __global__ __launch_bounds__(NW * 64, 1) void attn_bf16_pipe_kernel(AttnArgs a) 
     for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
       for (int e = 0; e < 16; ++e) m = fmaxf(m, s[kt][e]);
-    return max_halves(m) * sc;
+    return max_halves(m);
   };
 
   // prologue: tiles 0..3 in flight; tiles 0 and 1 landed before the loop
@@ -433,16 +442,19 @@ __global__ __launch_bounds__(NW * 64, 1) void attn_bf16_pipe_kernel(AttnArgs a) 
   float mcur = rowmax(scur);
 
   for (int j = 0; j < nkv; ++j) {
-    // lazy rescale for tile j
-    if (m_run == -INFINITY) {
-      m_run = mcur;
-    } else if (__builtin_amdgcn_ballot_w64(mcur > m_run + TAU) != 0) {
-      const float m_new = fmaxf(m_run, mcur);
-      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+    // lazy rescale for tile j (mcur is its row max relative to m_run): the
+    // first tile sets the max; later, only a lead of more than TAU moves it
+    // (then O^T, l and the tile's scores shift by the lead)
+    if (first || __builtin_amdgcn_ballot_w64(mcur > TAU) != 0) {
+      const float delta = first ? mcur : fmaxf(mcur, 0.f);
+      const float alpha = __builtin_amdgcn_exp2f(-delta);
       l_run *= alpha;
 #pragma unroll
       for (int t = 0; t < C::DT; ++t) oacc[t] *= alpha;
-      m_run = m_new;
+#pragma unroll
+      for (int kt = 0; kt < 2; ++kt) scur[kt] -= delta;
+      m_run += delta;
+      first = false;
     }
     // Softmax of tile j interleaved by hand with the QK^T MFMAs of tile j+1
     // (unconditional: the last iteration recomputes the last tile, unused):
@@ -452,22 +464,12 @@ __global__ __launch_bounds__(NW * 64, 1) void attn_bf16_pipe_kernel(AttnArgs a) 
     {
       const int tn = min(j + 1, nkv - 1), kvn = tn * C::BKV;
       const unsigned char* sln = smem + (tn % ST) * C::SLOT;
-#pragma unroll
-      for (int kt = 0; kt < 2; ++kt) {
-        f32x16 init = f32x16{};
-        if (kvn + C::BKV > Tj) {
-#pragma unroll
-          for (int e = 0; e < 16; ++e)
-            init[e] = kvn + kt * 32 + (e >> 2) * 8 + g * 4 + (e & 3) < Tj ? 0.f : -INFINITY;
-        }
-        snext[kt] = init;
-      }
+      s_init(kvn, snext);
       constexpr int NQ = 2 * C::KS;  // QK^T MFMAs per tile; MFMA i: half i % 2, k-step i / 2
       auto kread = [&](int i) { return *(const bf16x8*)(sln + (i & 1) * 32 * C::KROW + k_off[i >> 1]); };
       bf16x8 kf[3];
       kf[0] = kread(0);
       kf[1] = kread(1);
-      const float mneg = -m_run;
       float lsum = 0.f;
 #pragma unroll
       for (int i = 0; i < NQ; ++i) {
@@ -475,7 +477,7 @@ __global__ __launch_bounds__(NW * 64, 1) void attn_bf16_pipe_kernel(AttnArgs a) 
         snext[i & 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[i % 3], qf[i >> 1], snext[i & 1], 0, 0, 0);
 #pragma unroll
         for (int e = i * 32 / NQ; e < (i + 1) * 32 / NQ; ++e) {
-          const float p = __builtin_amdgcn_exp2f(fmaf(scur[e >> 4][e & 15], sc, mneg));
+          const float p = __builtin_amdgcn_exp2f(scur[e >> 4][e & 15]);
           scur[e >> 4][e & 15] = p;
           lsum += p;
         }
@@ -515,7 +517,7 @@ __global__ __launch_bounds__(NW * 64, 1) void attn_bf16_pipe_kernel(AttnArgs a) 
         for (int e = i * 32 / NP; e < (i + 1) * 32 / NP; ++e) m = fmaxf(m, snext[e >> 4][e & 15]);
         __builtin_amdgcn_sched_barrier(0);
       }
-      mcur = max_halves(m) * sc;
+      mcur = max_halves(m);
     }
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt) scur[kt] = snext[kt];

@@ -388,6 +388,7 @@ dit_status run_block(const dit_shape* s, const Layout& L, char* ws, StreamIO* io
       p.head_dim = dh;
       p.hidden = D;
       p.qk_stride = (int)L.qk;
+      p.k_scale = (float)(1.4426950408889634 / sqrt((double)dh));
     }
     G.flops = 2.0 * tokens * 3 * D * D;
     G.bytes = (tokens * D + ns * 3.0 * D * D + tokens * 3 * D) * E;
@@ -412,7 +413,8 @@ dit_status run_block(const dit_shape* s, const Layout& L, char* ws, StreamIO* io
     a.T_txt = ns > 1 ? io[1].Ts : 0;
     a.D = D;
     a.scale = 1.0f / sqrtf((float)dh);
-    a.scale_log2 = (float)(1.4426950408889634 / sqrt((double)dh));
+    // the bf16 QKV epilogue stores k already in the exp2 domain
+    a.scale_log2 = dt == DIT_BF16 ? 1.0f : (float)(1.4426950408889634 / sqrt((double)dh));
     const double flops = 4.0 * B * H * (double)L.Tj * L.Tj * dh;
     const double bytes = 4.0 * B * (double)L.Tj * D * E;
     HIP_TRY(timed(DIT_K_ATTENTION, flops, bytes, st, [&]() {

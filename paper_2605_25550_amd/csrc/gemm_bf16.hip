@@ -200,7 +200,8 @@ struct Epilogue {
         const int h = div_exact(rem, dh, 1.0f / (float)dh), d = rem - h * dh;
         const int b = div_exact(m, rpb, inv_rpb), jp = m - b * rpb + P.seq_off;
         bf16_t* dst = (bf16_t*)(s == 0 ? P.q : P.k) + (((long)b * P.heads + h) * P.Tj + jp) * P.qk_stride + d;
-        *(u32x2*)dst = u32x2{pack_bf16x2(y0, y1), pack_bf16x2(y2, y3)};
+        const float f = s == 0 ? 1.0f : P.k_scale;  // k in the softmax's exp2 domain, rounded once
+        *(u32x2*)dst = u32x2{pack_bf16x2(y0 * f, y1 * f), pack_bf16x2(y2 * f, y3 * f)};
         if (d + 4 == dh && P.qk_stride > dh)  // zero the row's padding (head_dim 72 -> 80)
           for (int z = 4; z < P.qk_stride - dh + 4; z += 4) *(u32x2*)(dst + z) = u32x2{0u, 0u};
       }

@@ -36,6 +36,7 @@ struct GemmProb {
   void* v;             // bf16: v^T [B, H, dh, Tj_pad], key j at column v_key_pos(j); fp32: [B, H, Tj, dh]
   int seq_off, Tj, Tj_pad, heads, head_dim, hidden;
   int qk_stride;       // q/k row length: head_dim, or (bf16) head_dim rounded up to 16, zero padded
+  float k_scale;       // bf16: k is stored multiplied by this (log2(e)/sqrt(dh), the softmax's exp2 scale)
 };
 
 struct GemmArgs {
@@ -58,7 +59,7 @@ struct AttnArgs {
   const void* v;   // bf16: v^T [B, H, dh, Tj_pad] (key j at column v_key_pos(j)); fp32: [B, H, Tj, dh]
   void* o;         // stream-major rows: image b*T + t, then text B*T + b*Tt + t; [*, H*dh]
   int B, H, Tj, Tj_pad, T_img, T_txt, D;
-  float scale_log2;  // log2(e) / sqrt(dh)
+  float scale_log2;  // factor from q.k to the exp2 domain: log2(e) / sqrt(dh), or 1 where k is stored pre-scaled (bf16)
   float scale;       // 1 / sqrt(dh)
 };
 
