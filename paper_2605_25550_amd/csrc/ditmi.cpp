@@ -241,66 +241,6 @@ hipError_t run_gemm(Gemm& G, int dtype, hipStream_t st) {
   });
 }
 
-// ------------------------------------------------------------------ weight prefetch
-// A side stream per (thread, device) reads the next block's GEMM weights
-// while the current block computes, so that they come from the Infinity
-// Cache rather than HBM.  The main stream never waits for it except once at
-// the end of a step call (so the caller may release the weights afterwards).
-struct SideStream {
-  int device = -1;
-  hipStream_t st = nullptr;
-  hipEvent_t ev_main = nullptr, ev_side = nullptr;
-};
-thread_local std::vector<SideStream> t_side;
-
-SideStream* side_stream() {
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess) return nullptr;
-  for (SideStream& s : t_side)
-    if (s.device == dev) return s.st ? &s : nullptr;
-  SideStream s;
-  s.device = dev;
-  if (hipStreamCreateWithFlags(&s.st, hipStreamNonBlocking) != hipSuccess ||
-      hipEventCreateWithFlags(&s.ev_main, hipEventDisableTiming) != hipSuccess ||
-      hipEventCreateWithFlags(&s.ev_side, hipEventDisableTiming) != hipSuccess) {
-    (void)hipGetLastError();
-    s.st = nullptr;  // prefetch is advisory: run without it
-  }
-  t_side.push_back(s);
-  return t_side.back().st ? &t_side.back() : nullptr;
-}
-
-// Enqueue on the side stream, after everything already enqueued on `main`, a
-// read of the four GEMM weight matrices of one block (all streams).
-hipError_t prefetch_weights(SideStream* ss, const dit_block_weights& b, const dit_shape* s, hipStream_t main) {
-  const size_t E = s->dtype == DIT_BF16 ? 2 : 4, D = s->hidden, F = s->mlp_hidden;
-  PrefetchArgs a{};
-  auto add = [&](const void* p, size_t bytes) {
-    a.p[a.n] = p;
-    a.bytes[a.n] = bytes / 64 * 64;
-    ++a.n;
-  };
-  const dit_stream_weights* st[2] = {&b.img, &b.txt};
-  for (int i = 0; i < (s->text_tokens > 0 ? 2 : 1); ++i) {
-    add(st[i]->w_qkv, 3 * D * D * E);
-    add(st[i]->w_o, D * D * E);
-    add(st[i]->w_fc1, F * D * E);
-    add(st[i]->w_fc2, D * F * E);
-  }
-  hipError_t e = hipEventRecord(ss->ev_main, main);
-  if (e == hipSuccess) e = hipStreamWaitEvent(ss->st, ss->ev_main, 0);
-  if (e == hipSuccess) e = launch_prefetch(a, ss->st);
-  return e;
-}
-
-// Prefetching pays while a block's GEMM weights fit in the 256 MB Infinity
-// Cache next to the activations; beyond that it only evicts useful lines.
-bool prefetch_pays(const dit_shape* s) {
-  const double E = s->dtype == DIT_BF16 ? 2 : 4, D = s->hidden, F = s->mlp_hidden;
-  const double per_block = (s->text_tokens > 0 ? 2 : 1) * (4 * D * D + 2 * F * D) * E;
-  return s->n_blocks > 1 && per_block <= 64.0 * (1 << 20);
-}
-
 // ------------------------------------------------------------------ block sequence
 struct StreamIO {
   const dit_stream_weights* w;
@@ -315,14 +255,7 @@ struct StreamIO {
     if (_e != hipSuccess) return fail(DIT_ERR_HIP, "%s: %s", #expr, hipGetErrorString(_e)); \
   } while (0)
 
-// Weights of the next block to read on the side stream while this one runs.
-struct NextBlock {
-  SideStream* ss;
-  const dit_block_weights* w;
-};
-
-dit_status run_block(const dit_shape* s, const Layout& L, char* ws, StreamIO* io, int ns, hipStream_t st,
-                     const NextBlock* next = nullptr) {
+dit_status run_block(const dit_shape* s, const Layout& L, char* ws, StreamIO* io, int ns, hipStream_t st) {
   const int B = s->batch, D = s->hidden, F = s->mlp_hidden, H = s->heads, dh = s->head_dim;
   const int dt = s->dtype;
   const size_t E = dt == DIT_BF16 ? 2 : 4;
@@ -394,10 +327,6 @@ dit_status run_block(const dit_shape* s, const Layout& L, char* ws, StreamIO* io
     G.bytes = (tokens * D + ns * 3.0 * D * D + tokens * 3 * D) * E;
     HIP_TRY(run_gemm(G, dt, st));
   }
-  // The next block's weight read starts once this block's QKV weights are
-  // consumed: earlier it competes with the QKV GEMM for HBM (measured: 1.8%
-  // of the step at DiT-XL/2 sizes against a prefetch at the block start).
-  if (next) HIP_TRY(prefetch_weights(next->ss, *next->w, s, st));
   // (3) o = softmax(q k^T / sqrt(dh)) v over the joint sequence
   {
     AttnArgs a{};
@@ -561,21 +490,11 @@ dit_status run_step(const dit_shape* s, const dit_step_weights* w, const Layout&
     return launch_patch_embed(B * T, T, s->patch_in, D, patches, w->w_patch, w->b_patch, w->pos, x, s->dtype, hs);
   }));
 
-  // (a4-a11) blocks.  The GEMM weights of block l+1 are read into the
-  // Infinity Cache on the side stream while block l runs, from its attention
-  // on (block 0's during the embedding).  Measured: about 6% of the step at
-  // DiT-XL/2 sizes.
-  SideStream* ss = prefetch_pays(s) ? side_stream() : nullptr;
-  if (ss) HIP_TRY(prefetch_weights(ss, w->blocks[0], s, hs));
+  // (a4-a11) blocks
   for (int l = 0; l < s->n_blocks; ++l) {
-    const NextBlock next{ss, l + 1 < s->n_blocks ? &w->blocks[l + 1] : nullptr};
     StreamIO io[2] = {{&w->blocks[l].img, x, mod + (size_t)(l * ns) * per, T},
                       {&w->blocks[l].txt, x_txt, mod + (size_t)(l * ns + 1) * per, s->text_tokens}};
-    if ((st = run_block(s, L, ws, io, ns, hs, ss && next.w ? &next : nullptr)) != DIT_OK) return st;
-  }
-  if (ss) {  // join: later work on the caller's stream is ordered after every prefetch
-    HIP_TRY(hipEventRecord(ss->ev_side, ss->st));
-    HIP_TRY(hipStreamWaitEvent(hs, ss->ev_side, 0));
+    if ((st = run_block(s, L, ws, io, ns, hs)) != DIT_OK) return st;
   }
 
   // (a12) out = (LN(x) * (1 + scale_f) + shift_f) W_final^T + b_final, image tokens only

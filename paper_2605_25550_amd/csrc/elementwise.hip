@@ -443,47 +443,5 @@ hipError_t launch_axpy_f32(float* z, const float* v, float a, long n, hipStream_
   return hipGetLastError();
 }
 
-// ---------------------------------------------------------------- weight prefetch
-// Touches one dword of every 64-byte line of up to PREFETCH_MAX regions so
-// that they are resident in the memory-side Infinity Cache when the next
-// block's GEMMs stream them (plain loads: non-temporal ones were measured
-// not to stay resident).  The loaded values are discarded.
-__global__ __launch_bounds__(256) void prefetch_kernel(PrefetchArgs a) {
-  unsigned acc = 0;
-  const size_t start = ((size_t)blockIdx.x * 256 + threadIdx.x) * 64;
-  const size_t stride = (size_t)gridDim.x * 256 * 64;
-#pragma unroll
-  for (int r = 0; r < PREFETCH_MAX; ++r) {
-    if (r >= a.n) break;
-    const char* base = (const char*)a.p[r];
-    const size_t n = a.bytes[r];
-    size_t off = start;
-    for (; off + 7 * stride < n; off += 8 * stride) {
-      unsigned v[8];
-#pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const unsigned* q = (const unsigned*)(base + off + u * stride);
-        v[u] = *q;
-      }
-#pragma unroll
-      for (int u = 0; u < 8; ++u) acc += v[u];
-    }
-    for (; off < n; off += stride) {
-      const unsigned* q = (const unsigned*)(base + off);
-      acc += *q;
-    }
-  }
-  asm volatile("" : : "v"(acc));  // keep the loads
-}
-
-// 64 workgroups x 256 lanes x 8 lines in flight: the read finishes early in
-// the block (a 16-workgroup grid, streaming for longer, was measured to slow
-// the overlapped GEMMs far more).
-constexpr int PREFETCH_WGS = 64;
-hipError_t launch_prefetch(const PrefetchArgs& a, hipStream_t st) {
-  if (a.n <= 0) return hipSuccess;
-  hipLaunchKernelGGL(prefetch_kernel, dim3(PREFETCH_WGS), dim3(256), 0, st, a);
-  return hipGetLastError();
-}
 
 }  // namespace ditmi

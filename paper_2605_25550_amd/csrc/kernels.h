@@ -93,14 +93,6 @@ struct AdaArgs {
   int B, D;
 };
 
-// ------------------------------------------------------------------ weight prefetch
-constexpr int PREFETCH_MAX = 8;
-struct PrefetchArgs {
-  const void* p[PREFETCH_MAX];
-  size_t bytes[PREFETCH_MAX];   // region sizes; whole 64-byte lines are touched
-  int n;
-};
-
 // ------------------------------------------------------------------ launchers
 // Each returns hipSuccess or the launch error.  dtype: 0 = fp32, 1 = bf16.
 hipError_t launch_gemm_bf16(const GemmArgs& a, int epi, int tile_cfg, hipStream_t st);
@@ -117,7 +109,6 @@ hipError_t launch_cond_embed(int B, int D, const float* t, const int32_t* y, con
 hipError_t launch_patch_embed(int rows, int T, int P, int D, const float* z, const void* w, const void* b,
                               const float* pos, float* x, int dtype, hipStream_t st);
 hipError_t launch_pos_embed_2d(int gh, int gw, int D, float* pos, hipStream_t st);
-hipError_t launch_prefetch(const PrefetchArgs& a, hipStream_t st);
 hipError_t launch_fill_f32(float* p, int n, float v, hipStream_t st);
 // z[i] += a * v[i], i < n; n a multiple of 4, both 16-byte aligned
 hipError_t launch_axpy_f32(float* z, const float* v, float a, long n, hipStream_t st);
