@@ -193,13 +193,15 @@ __global__ __launch_bounds__(256) void adaln_kernel(AdaArgs a) {
 
 // bf16 weights: the same product on v_mfma_f32_16x16x32_bf16 as
 // out^T [N, B] = W [N, K] * SiLU(c)^T [K, B].  A workgroup (4 waves x 2 row
-// tiles of 16) owns 128 rows of one entry.  A-operand lanes read their 16
-// bytes of W straight from global memory (row lane%16, k offset 8*(lane/16));
-// the B operand, SiLU(c) in bf16 for 16 samples (computed once by
-// silu_bf16_kernel, zero rows past the batch), is copied to LDS with a
-// 16-byte row pad so that the 16 rows read by a quarter-wave fall on distinct
-// banks.  Batches above 16 loop over 16-sample tiles.  D lanes hold column
-// (sample) lane%16, rows 4*(lane/16) + i.
+// tiles of 16) owns 128 rows of one entry.  Both operands are read straight
+// from global memory, 16 bytes per lane (row lane%16, k offset 8*(lane/16)):
+// W streams from HBM once, and the B operand, SiLU(c) in bf16 for 16 samples
+// (computed once by silu_bf16_kernel, zero rows past the batch; at most a
+// few hundred KB), stays in L2.  No LDS, so many workgroups share a CU and
+// keep enough weight loads in flight to stream HBM (staging the B operand
+// in LDS held one workgroup per CU at hidden 3072).  Batches above 16 loop
+// over 16-sample tiles.  D lanes hold column (sample) lane%16, rows
+// 4*(lane/16) + i.
 __global__ void silu_bf16_kernel(int B, int D, int rows, const float* cond, bf16_t* act) {
   const long idx = (long)blockIdx.x * blockDim.x + threadIdx.x;
   if (idx >= (long)rows * D) return;
@@ -216,13 +218,12 @@ hipError_t launch_silu_bf16(int B, int D, const float* cond, void* act, hipStrea
 }
 
 __global__ __launch_bounds__(256) void adaln_mfma_kernel(AdaArgs a) {
-  extern __shared__ __attribute__((aligned(16))) bf16_t sact[];  // [16][K + 8]
   const int wg = blockIdx.x;
   int ei = 0;
   while (ei + 1 < a.ne && wg >= a.e[ei + 1].wg_begin) ++ei;
   const AdaEntry& E = a.e[ei];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int K = a.D, SST = K + 8, N = E.N, cpr = K >> 3;
+  const int K = a.D, N = E.N;
   const int nbase = (wg - E.wg_begin) * 128 + wave * 32;
   const bf16_t* __restrict__ W = (const bf16_t*)E.W;
   const bf16_t* __restrict__ bias = (const bf16_t*)E.bias;
@@ -230,17 +231,11 @@ __global__ __launch_bounds__(256) void adaln_mfma_kernel(AdaArgs a) {
   const int r16 = lane & 15, kq = lane >> 4;
   const bf16_t* w0 = W + (long)min(nbase + r16, N - 1) * K + 8 * kq;
   const bf16_t* w1 = W + (long)min(nbase + 16 + r16, N - 1) * K + 8 * kq;
-  const bf16_t* sp = sact + r16 * SST + 8 * kq;
 
   for (int b0 = 0; b0 < a.B; b0 += 16) {
-    __syncthreads();
-    for (int i = tid; i < 16 * cpr; i += 256) {  // 16-byte chunks of 16 rows
-      const int r = i / cpr, c = i - r * cpr;
-      *(u32x4*)(sact + r * SST + 8 * c) = *(const u32x4*)(act + (long)(b0 + r) * K + 8 * c);
-    }
-    __syncthreads();
+    const bf16_t* sp = act + (long)(b0 + r16) * K + 8 * kq;
     f32x4 acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll 4
+#pragma unroll 8
     for (int k0 = 0; k0 < K; k0 += 32) {
       const bf16x8 a0 = *(const bf16x8*)(w0 + k0);
       const bf16x8 a1 = *(const bf16x8*)(w1 + k0);
@@ -265,11 +260,7 @@ __global__ __launch_bounds__(256) void adaln_mfma_kernel(AdaArgs a) {
 hipError_t launch_adaln(const AdaArgs& a, int dtype, hipStream_t st) {
   dim3 grid(a.total_wg), block(256);
   if (dtype == 1) {
-    const size_t lds = (size_t)16 * (a.D + 8) * sizeof(bf16_t);
-    hipError_t e = hipFuncSetAttribute((const void*)adaln_mfma_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                       (int)lds);
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(adaln_mfma_kernel, grid, block, lds, st, a);
+    hipLaunchKernelGGL(adaln_mfma_kernel, grid, block, 0, st, a);
   } else {
     const size_t lds = (size_t)(a.B < 8 ? a.B : 8) * a.D * sizeof(float);
     hipError_t e = hipFuncSetAttribute((const void*)adaln_kernel<float>,
