@@ -31,13 +31,14 @@ PROFILES = os.path.join(ROOT, "profiles")
 
 # kernel class -> (regex of its kernel symbol in rocprofv3 output, source file).  The
 # GEMM classes differ in the last template argument (the fused epilogue), for
-# both GEMM kernels (gemm_bf16_kernel<BM, BN, STAGES, EPI>, gemm_bf16_144_kernel<EPI>).
+# both GEMM kernels (gemm_bf16_kernel<BM, BN, WGM, WGN, STAGES, EPI>,
+# gemm_bf16_144_kernel<EPI>).
 CLASSES = {
-    "gemm_qkv": (r"gemm_bf16_\w*kernel<(?:\d+, \d+, \d+, )?0>", "gemm_bf16.hip"),
+    "gemm_qkv": (r"gemm_bf16_\w*kernel<(?:\d+, )*0>", "gemm_bf16.hip"),
     "attention": (r"attn_bf16_\w*kernel<", "attention_bf16.hip"),
-    "gemm_out": (r"gemm_bf16_\w*kernel<(?:\d+, \d+, \d+, )?2>", "gemm_bf16.hip"),
-    "gemm_fc1": (r"gemm_bf16_\w*kernel<(?:\d+, \d+, \d+, )?1>", "gemm_bf16.hip"),
-    "gemm_fc2": (r"gemm_bf16_\w*kernel<(?:\d+, \d+, \d+, )?4>", "gemm_bf16.hip"),
+    "gemm_out": (r"gemm_bf16_\w*kernel<(?:\d+, )*2>", "gemm_bf16.hip"),
+    "gemm_fc1": (r"gemm_bf16_\w*kernel<(?:\d+, )*1>", "gemm_bf16.hip"),
+    "gemm_fc2": (r"gemm_bf16_\w*kernel<(?:\d+, )*4>", "gemm_bf16.hip"),
     "ln_mod": (r"ln_mod_kernel<", "elementwise.hip"),
     "adaln": (r"adaln_kernel<", "elementwise.hip"),
 }
