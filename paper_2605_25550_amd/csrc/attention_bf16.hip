@@ -32,8 +32,10 @@
 // from overflowing the fp32 sums, so after the first tile the rescale (which
 // touches every accumulator) practically never runs.
 //
-// head_dim 72 uses q and k rows zero-padded to 80 (written that way by the
-// QKV epilogue) for the k-steps of 16, and 96 rows of V^T (rows 72..95 zero).
+// head_dim 72 uses q and k rows padded to 80 (written that way by the QKV
+// epilogue: zeros, except k's column 72 = 1) for the k-steps of 16, and 96
+// rows of V^T (rows 72..95 kept in LDS only).  The pipelined kernel below uses
+// that padding to move softmax bookkeeping into the MFMAs (AttnCfg::FOLD).
 #include "common.h"
 #include "kernels.h"
 
@@ -59,7 +61,17 @@ struct AttnCfg {
   }
   static __device__ __forceinline__ int swz_v(int d) { return (d >> 1) & 7; }
   static_assert(KTILE % 1024 == 0 && DH * 128 % 1024 == 0, "tiles are whole 1 KB DMA blocks");
+  // Softmax bookkeeping folded into the MFMAs (head_dim 72: padding column
+  // DH of k holds 1, so q's column DH carries -m_run into S^T; padding row DH
+  // of V^T holds ones, so O^T row DH accumulates the row sum l).
+  static constexpr bool FOLD = DHP > DH && VROWS > DH + 4 && DH % 32 % 8 < 4;
+  static constexpr int QS = DH / 16, QG = (DH % 16) / 8, QE = DH % 8;  // q register slot of column DH
+  static constexpr int LT = DH / 32, LG = (DH % 32) % 8 / 4, LE = (DH % 32) / 8 * 4 + DH % 4;  // O^T slot of row DH
+  // ring depth of the pipelined kernel (measured: deeper rings, where they
+  // fit, were not faster)
+  static constexpr int PIPE_ST = 4;
 };
+
 
 template <int DH, int NW, int QT>
 __global__ __launch_bounds__(NW * 64, QT == 1 ? 8 / NW : 1) void attn_bf16_dma_kernel(AttnArgs a) {
@@ -291,10 +303,11 @@ __global__ __launch_bounds__(NW * 64, QT == 1 ? 8 / NW : 1) void attn_bf16_dma_k
 // slots (tile t in slot t % 4, refilled with t + 4 after the barrier that
 // ends iteration t), which keeps two iterations between a tile's DMA and its
 // first read.
-template <int DH, int NW>
-__global__ __launch_bounds__(NW * 64, 1) void attn_bf16_pipe_kernel(AttnArgs a) {
+template <int DH, int NW, int ST = AttnCfg<DH>::PIPE_ST, int WPC = 1>
+__global__ __launch_bounds__(NW * 64, WPC) void attn_bf16_pipe_kernel(AttnArgs a) {
   using C = AttnCfg<DH>;
-  constexpr int ST = 4;
+  constexpr bool FOLD = C::FOLD;
+  static_assert(ST >= 3 && WPC * (ST * C::SLOT + 1024) <= 160 * 1024, "ring fits the LDS");
   constexpr int IPW = (C::TDMA + NW - 1) / NW;  // DMA instructions per wave per tile (uniform)
   __shared__ __attribute__((aligned(1024))) unsigned char smem[ST * C::SLOT + 1024];
 
@@ -326,23 +339,34 @@ __global__ __launch_bounds__(NW * 64, 1) void attn_bf16_pipe_kernel(AttnArgs a) 
     const int vb = byte - C::KTILE, d = vb >> 7, pos = (vb & 127) >> 4;
     return (unsigned)((d * Tjp + min((pos ^ C::swz_v(d)) * 8, cmax)) * 2);
   };
-  unsigned doff[IPW];
+  // Lane offsets of a full tile and of the last tile (clamped where it is
+  // partial).
+  const int kv_last = (nkv - 1) * C::BKV;
+  unsigned doff[IPW], doff_last[IPW];
 #pragma unroll
-  for (int t = 0; t < IPW; ++t) doff[t] = dma_off(wave + NW * t < C::TDMA ? t : -1, C::BKV, C::BKV);
-  auto issue = [&](int tile) {
-    const int kv0 = tile * C::BKV;
-    const unsigned base = lds0 + (unsigned)((tile % ST) * C::SLOT);
+  for (int t = 0; t < IPW; ++t) {
+    const int tt = wave + NW * t < C::TDMA ? t : -1;
+    doff[t] = dma_off(tt, C::BKV, C::BKV);
+    doff_last[t] = dma_off(tt, Tj - 1 - kv_last, Tjp - 8 - kv_last);
+  }
+  // DMA instruction t of `tile` into slot tile % ST.  Past the last tile it
+  // re-reads the last tile into the spare line, so that every wave issues
+  // the same number of DMA instructions per iteration whatever the tile
+  // count, and the vmcnt waits are constants.
+  auto issue_one = [&](int tile, int t) {
+    const int qi = wave + NW * t;  // wave-uniform
+    const int tl = min(tile, nkv - 1), kv0 = tl * C::BKV;
     const bf16_t* kb = kp + (long)kv0 * C::DHP;  // wave-uniform
     const bf16_t* vb = vp + kv0;
-    const bool full = kv0 + C::BKV <= Tj;
+    const bool kpart = qi < C::KDMA || qi >= C::TDMA;
+    const unsigned off = tl == nkv - 1 ? doff_last[t] : doff[t];
+    const unsigned dst = tile < nkv && qi < C::TDMA ? lds0 + (unsigned)((tile % ST) * C::SLOT + qi * 1024)
+                                                     : lds0 + (unsigned)(ST * C::SLOT);
+    dma_16s(kpart ? (const void*)kb : (const void*)vb, off, dst);
+  };
+  auto issue = [&](int tile) {
 #pragma unroll
-    for (int t = 0; t < IPW; ++t) {
-      const int qi = wave + NW * t;  // wave-uniform
-      const bool kpart = qi < C::KDMA || qi >= C::TDMA;
-      const unsigned off = full ? doff[t] : dma_off(qi < C::TDMA ? t : -1, Tj - 1 - kv0, Tjp - 8 - kv0);
-      const unsigned dst = qi < C::TDMA ? base + (unsigned)(qi * 1024) : lds0 + (unsigned)(ST * C::SLOT);
-      dma_16s(kpart ? (const void*)kb : (const void*)vb, off, dst);
-    }
+    for (int t = 0; t < IPW; ++t) issue_one(tile, t);
   };
   // V^T columns of keys past the end (last tile only) hold stale workspace
   // bytes; zero them so that their zero probabilities cannot meet a NaN.
@@ -357,10 +381,12 @@ __global__ __launch_bounds__(NW * 64, 1) void attn_bf16_pipe_kernel(AttnArgs a) 
   };
 
   // V^T rows past head_dim (head_dim 72 only) are never written by the DMA.
+  // They are zero, except row DH, which is all ones where the row sums are
+  // folded into the PV product (O^T row DH = sum of the tile's P).
   if (C::VROWS > DH) {
     for (int e = tid; e < ST * (C::VROWS - DH) * 32; e += NW * 64) {
       const int sl = e / ((C::VROWS - DH) * 32), w = e % ((C::VROWS - DH) * 32);
-      ((uint32_t*)(smem + sl * C::SLOT + C::KTILE + DH * 128))[w] = 0u;
+      ((uint32_t*)(smem + sl * C::SLOT + C::KTILE + DH * 128))[w] = FOLD && w < 32 ? 0x3F803F80u : 0u;
     }
   }
 
@@ -378,9 +404,11 @@ __global__ __launch_bounds__(NW * 64, 1) void attn_bf16_pipe_kernel(AttnArgs a) 
 #pragma unroll
   for (int c = 0; c < 4; ++c) v_off[c] = C::KTILE + r32 * 128 + (((2 * c + g) ^ C::swz_v(r32)) << 4);
 
-  // k arrives in the exp2 domain (stored pre-scaled by the QKV epilogue), and
-  // every S^T accumulator starts at -m_run (the running max at the time its
-  // QK^T is issued), so the MFMA result is directly the exp2 argument.
+  // k arrives in the exp2 domain (stored pre-scaled by the QKV epilogue).
+  // The running max m_run is subtracted inside the QK^T product, so the MFMA
+  // result is directly the exp2 argument: with FOLD, k's padding column DH
+  // holds 1 and q's holds -m_run (kept exactly representable in bf16);
+  // otherwise every S^T accumulator starts at -m_run.
   const float TAU = 64.0f;  // lazy max, as in the kernel above
   float m_run = 0.f, l_run = 0.f;
   bool first = true;
@@ -388,26 +416,28 @@ __global__ __launch_bounds__(NW * 64, 1) void attn_bf16_pipe_kernel(AttnArgs a) 
 #pragma unroll
   for (int t = 0; t < C::DT; ++t) oacc[t] = f32x16{};
 
-  // S^T of one key tile minus m_run: accumulators start at -m_run, and at
-  // -inf for keys past the end.
-  auto s_init = [&](int kv0, f32x16 (&s)[2]) {
+  // S^T of one key tile minus m_run; s_mask sets keys past the end to -inf.
+  auto s_init = [&](f32x16 (&s)[2]) {
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt) {
       f32x16 init;
 #pragma unroll
-      for (int e = 0; e < 16; ++e) init[e] = -m_run;
-      if (kv0 + C::BKV > Tj) {
-#pragma unroll
-        for (int e = 0; e < 16; ++e)
-          if (kv0 + kt * 32 + (e >> 2) * 8 + g * 4 + (e & 3) >= Tj) init[e] = -INFINITY;
-      }
+      for (int e = 0; e < 16; ++e) init[e] = FOLD ? 0.f : -m_run;
       s[kt] = init;
     }
   };
+  auto s_mask = [&](int kv0, f32x16 (&s)[2]) {
+    if (kv0 + C::BKV > Tj) {
+#pragma unroll
+      for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+        for (int e = 0; e < 16; ++e)
+          if (kv0 + kt * 32 + (e >> 2) * 8 + g * 4 + (e & 3) >= Tj) s[kt][e] = -INFINITY;
+    }
+  };
   auto qk = [&](int tile, f32x16 (&s)[2]) {
-    const int kv0 = tile * C::BKV;
     const unsigned char* sl = smem + (tile % ST) * C::SLOT;
-    s_init(kv0, s);
+    s_init(s);
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
@@ -425,13 +455,11 @@ __global__ __launch_bounds__(NW * 64, 1) void attn_bf16_pipe_kernel(AttnArgs a) 
     return max_halves(m);
   };
 
-  // prologue: tiles 0..3 in flight; tiles 0 and 1 landed before the loop
+  // prologue: tiles 0 .. ST-2 in flight (tile ST-1 is issued in the first
+  // iteration); tiles 0 and 1 landed before the loop
 #pragma unroll
-  for (int t = 0; t < ST; ++t)
-    if (t < nkv) issue(t);
-  if (nkv >= 4) wait_vmcnt<2 * IPW>();
-  else if (nkv == 3) wait_vmcnt<IPW>();
-  else wait_vmcnt<0>();
+  for (int t = 0; t < ST - 1; ++t) issue(t);
+  wait_vmcnt<(ST - 3) * IPW>();
   __syncthreads();
   if (nkv <= 2) {  // the last tile has landed already (else: zeroed at the end of iteration nkv-3)
     zero_v_tail(nkv - 1);
@@ -442,29 +470,40 @@ __global__ __launch_bounds__(NW * 64, 1) void attn_bf16_pipe_kernel(AttnArgs a) 
   float mcur = rowmax(scur);
 
   for (int j = 0; j < nkv; ++j) {
+    // Keys past the end (last tile only) are masked just before their
+    // exponentials.  Their K rows repeat row Tj-1, so the unmasked row max
+    // taken earlier is still the max over real keys.
+    s_mask(j * C::BKV, scur);
     // lazy rescale for tile j (mcur is its row max relative to m_run): the
     // first tile sets the max; later, only a lead of more than TAU moves it
     // (then O^T, l and the tile's scores shift by the lead)
     if (first || __builtin_amdgcn_ballot_w64(mcur > TAU) != 0) {
-      const float delta = first ? mcur : fmaxf(mcur, 0.f);
+      float m_new = m_run + (first ? mcur : fmaxf(mcur, 0.f));
+      if (FOLD) m_new = bf2f(f2bf(m_new));  // enters the product as a bf16 operand
+      const float delta = m_new - m_run;     // exact
       const float alpha = __builtin_amdgcn_exp2f(-delta);
-      l_run *= alpha;
+      if (!FOLD) l_run *= alpha;
 #pragma unroll
       for (int t = 0; t < C::DT; ++t) oacc[t] *= alpha;
 #pragma unroll
       for (int kt = 0; kt < 2; ++kt) scur[kt] -= delta;
-      m_run += delta;
+      m_run = m_new;
+      if (FOLD && g == C::QG) qf[C::QS][C::QE] = __builtin_bit_cast(__bf16, f2bf(-m_run));
       first = false;
     }
     // Softmax of tile j interleaved by hand with the QK^T MFMAs of tile j+1
     // (unconditional: the last iteration recomputes the last tile, unused):
     // K fragments are read two MFMAs ahead, the MFMAs alternate between the
     // two 32-key halves (independent accumulators), and each MFMA is
-    // followed by its share of the exponentials.
+    // followed by its share of the exponentials.  The DMA of tile j+ST-1
+    // into the slot of tile j-1 (released by the last barrier) is spread
+    // over the same sequence: issued as a burst after the barrier, the
+    // workgroup's DMA instructions queue at the address unit and stall the
+    // waves at issue.
     {
       const int tn = min(j + 1, nkv - 1), kvn = tn * C::BKV;
       const unsigned char* sln = smem + (tn % ST) * C::SLOT;
-      s_init(kvn, snext);
+      s_init(snext);
       constexpr int NQ = 2 * C::KS;  // QK^T MFMAs per tile; MFMA i: half i % 2, k-step i / 2
       auto kread = [&](int i) { return *(const bf16x8*)(sln + (i & 1) * 32 * C::KROW + k_off[i >> 1]); };
       bf16x8 kf[3];
@@ -476,14 +515,17 @@ __global__ __launch_bounds__(NW * 64, 1) void attn_bf16_pipe_kernel(AttnArgs a) 
         if (i + 2 < NQ) kf[(i + 2) % 3] = kread(i + 2);
         snext[i & 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[i % 3], qf[i >> 1], snext[i & 1], 0, 0, 0);
 #pragma unroll
+        for (int t = 0; t < IPW; ++t)
+          if (i == 1 + t * (NQ - 1) / IPW) issue_one(j + ST - 1, t);
+#pragma unroll
         for (int e = i * 32 / NQ; e < (i + 1) * 32 / NQ; ++e) {
           const float p = __builtin_amdgcn_exp2f(scur[e >> 4][e & 15]);
           scur[e >> 4][e & 15] = p;
-          lsum += p;
+          if (!FOLD) lsum += p;
         }
         __builtin_amdgcn_sched_barrier(0);
       }
-      l_run += lsum;
+      if (!FOLD) l_run += lsum;
     }
     u32x4 pw[4];
 #pragma unroll
@@ -522,11 +564,10 @@ __global__ __launch_bounds__(NW * 64, 1) void attn_bf16_pipe_kernel(AttnArgs a) 
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt) scur[kt] = snext[kt];
     // tile j+2 must have landed for every wave before the next iteration's
-    // QK^T; every wave is done with slot j % ST, which takes tile j+4
-    if (j + 3 < nkv) wait_vmcnt<IPW>();
-    else wait_vmcnt<0>();
+    // QK^T (tiles j+3 .. j+ST-1 may still be in flight), and every wave must
+    // be done with slot j % ST before it takes tile j+ST
+    wait_vmcnt<(ST - 3) * IPW>();
     __syncthreads();
-    if (j + 4 < nkv) issue(j + 4);
     if (j + 2 == nkv - 1) {  // the last tile's V^T is read in iteration nkv-1
       zero_v_tail(nkv - 1);
       __syncthreads();
@@ -536,7 +577,10 @@ __global__ __launch_bounds__(NW * 64, 1) void attn_bf16_pipe_kernel(AttnArgs a) 
 
   {
     const int qrow = q0 + r32;
-    const float inv = 1.0f / sum_halves(l_run);
+    // with FOLD, l is O^T row DH: element LE of tile LT in the lanes of half
+    // LG (the other half holds a zero row there)
+    const float l_lane = FOLD ? (g == C::LG ? oacc[C::LT][C::LE] : 0.f) : l_run;
+    const float inv = 1.0f / sum_halves(l_lane);
     if (qrow < Tj) {
       const long orow = qrow < a.T_img ? (long)b * a.T_img + qrow
                                        : (long)a.B * a.T_img + (long)b * a.T_txt + (qrow - a.T_img);

@@ -202,42 +202,47 @@ struct Epilogue {
         bf16_t* dst = (bf16_t*)(s == 0 ? P.q : P.k) + (((long)b * P.heads + h) * P.Tj + jp) * P.qk_stride + d;
         const float f = s == 0 ? 1.0f : P.k_scale;  // k in the softmax's exp2 domain, rounded once
         *(u32x2*)dst = u32x2{pack_bf16x2(y0 * f, y1 * f), pack_bf16x2(y2 * f, y3 * f)};
-        if (d + 4 == dh && P.qk_stride > dh)  // zero the row's padding (head_dim 72 -> 80)
-          for (int z = 4; z < P.qk_stride - dh + 4; z += 4) *(u32x2*)(dst + z) = u32x2{0u, 0u};
+        // The row's padding (head_dim 72 -> 80) is zero, except k's column
+        // head_dim, which is 1: there the attention kernel folds the running
+        // softmax max into the QK^T product.
+        if (d + 4 == dh && P.qk_stride > dh)
+          for (int z = 4; z < P.qk_stride - dh + 4; z += 4)
+            *(u32x2*)(dst + z) = u32x2{s == 1 && z == 4 ? 0x3F80u : 0u, 0u};
       }
     }
   }
 };
 
-template <int BM, int BN, int WGM, int WGN, int STAGES, int EPI>
-__global__ __launch_bounds__(WGM * WGN * 64) void gemm_bf16_kernel(GemmArgs args) {
-  using C = GemmCfg<BM, BN, WGM, WGN, STAGES>;
-  __shared__ __attribute__((aligned(1024))) unsigned char smem[C::LDS];
-
-  const int tile = xcd_remap(blockIdx.x, args.total_tiles);
-  // Select the problem by value: indexing the by-value argument array with a
-  // runtime index would copy it to scratch memory.
-  const bool second = args.nprob > 1 && tile >= args.p[1].tile_begin;
-  const GemmProb P = second ? args.p[1] : args.p[0];
-  const int local = tile - P.tile_begin;
+// Tile `local` of problem P -> its first row and column.  Tiles are taken in
+// groups of 8 M-tiles x all N-tiles, M fastest within a group, so that
+// consecutive tiles share W columns and a group's A rows stay in one L2.
+template <int BM, int BN>
+__device__ __forceinline__ void tile_origin(const GemmProb& P, int local, int& m0, int& n0) {
   const int GM = 8;
   const int group_size = GM * P.tiles_n;
   const int group = local / group_size;
   const int first_m = group * GM;
   const int gm = min(P.tiles_m - first_m, GM);
   const int in_group = local - group * group_size;
-  const int m0 = (first_m + in_group % gm) * BM;
-  const int n0 = (in_group / gm) * BN;
+  m0 = (first_m + in_group % gm) * BM;
+  n0 = (in_group / gm) * BN;
+}
 
-  const bf16_t* __restrict__ A = (const bf16_t*)P.A;
-  const bf16_t* __restrict__ W = (const bf16_t*)P.W;
+// Main loop of one tile over the k-slices kb .. kb+nks-1 (nks >= 1) into acc,
+// which it zeroes first.  On return every wave's DMA has landed and its LDS
+// reads of the ring are complete, but other waves may still be reading: a
+// workgroup barrier must precede any reuse of the LDS.
+template <int BM, int BN, int WGM, int WGN, int STAGES>
+__device__ __forceinline__ void gemm_mainloop(const GemmProb& P, int m0, int n0, int kb, int nks,
+                                              f32x16 (&acc)[BM / WGM / 32][BN / WGN / 32],
+                                              unsigned char* smem, unsigned lds0, int wave, int lane) {
+  using C = GemmCfg<BM, BN, WGM, WGN, STAGES>;
+  const bf16_t* __restrict__ A = (const bf16_t*)P.A + (long)kb * C::BK;
+  const bf16_t* __restrict__ W = (const bf16_t*)P.W + (long)kb * C::BK;
   const int M = P.M, N = P.N, K = P.K;
-  const int KT = K / C::BK;
-  const int tid = threadIdx.x, lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform (scalar) index
+  const int KT = nks;
   const int wm = wave / WGN, wn = wave - wm * WGN;
   const int r32 = lane & 31, g = lane >> 5;
-  const unsigned lds0 = __builtin_amdgcn_readfirstlane(lds_address(smem));
 
   // DMA instruction t of this wave fills slice rows 8q .. 8q+7, q = wave + NW t;
   // lane -> row 8q + lane/8 at stored position lane%8, which holds chunk
@@ -277,7 +282,6 @@ __global__ __launch_bounds__(WGM * WGN * 64) void gemm_bf16_kernel(GemmArgs args
     }
   }
 
-  f32x16 acc[C::TM][C::TN];
 #pragma unroll
   for (int i = 0; i < C::TM; ++i)
 #pragma unroll
@@ -309,15 +313,6 @@ __global__ __launch_bounds__(WGM * WGN * 64) void gemm_bf16_kernel(GemmArgs args
     }                                                                                        \
     _Pragma("unroll") for (int q = C::TM * C::TN; q < (ND); ++q) if (ON) dma_one(DSL, DSLOT, (T0) + q); \
   } while (0)
-
-  // Epilogue constants (bias, gate) are requested first, so they are resident
-  // long before the epilogue; being older than every DMA, they never delay
-  // the explicit vmcnt waits below.
-  using E = Epilogue<EPI, C::WTN, C::CST>;
-  const int nw0 = n0 + wn * C::WTN;
-  const bool vcols = EPI == EPI_QKV && n0 >= 2 * P.hidden;  // tiles never straddle k|v (2D % BN == 0)
-  E epi;
-  epi.init(P, nw0, m0 + wm * C::WTM, vcols, lane);
 
   // Slices past the end are not issued; where fewer than the steady-state
   // number are in flight, the waits fall back to vmcnt(0).
@@ -371,19 +366,28 @@ __global__ __launch_bounds__(WGM * WGN * 64) void gemm_bf16_kernel(GemmArgs args
 #undef GEMM_MFMA
 #undef GEMM_MFMA_DMA
 #undef SCHED_FENCE
+}
 
-  // ---------------------------------------------------------------- epilogue
-  // Per 32-row slab i: each wave writes its 32 x WTN accumulators to its own
-  // LDS region (column r32 + 32j, rows 8*jj + 4*g + ii), then reads them back
-  // four columns (or, for v^T, four rows) per lane.  The residual rows of
-  // slab i+1 are requested before slab i is processed.
-  // A wave only reads back its own LDS region, and the LDS executes one
-  // wave's instructions in order, so after one workgroup barrier (every wave
-  // is done with the slice ring, which the regions overlap) the slabs need
-  // no further barriers, only a wavefront-scope fence that keeps the
-  // compiler from reordering the lanes' LDS writes and reads.
+// Epilogue of one tile from the accumulators.  Per 32-row slab i: each wave
+// writes its 32 x WTN accumulators to its own LDS region (column r32 + 32j,
+// rows 8*jj + 4*g + ii), then reads them back four columns (or, for v^T,
+// four rows) per lane.  The residual rows of slab i+1 are requested before
+// slab i is processed.  A wave only reads back its own LDS region, and the
+// LDS executes one wave's instructions in order, so after one workgroup
+// barrier (every wave is done with the slice ring, which the regions
+// overlap) the slabs need no further barriers, only a wavefront-scope fence
+// that keeps the compiler from reordering the lanes' LDS writes and reads.
+template <int BM, int BN, int WGM, int WGN, int STAGES, int EPI>
+__device__ __forceinline__ void gemm_epilogue(const GemmProb& P, int m0, int n0, bool vcols,
+                                              const Epilogue<EPI, BN / WGN, BN / WGN + 4>& epi,
+                                              const f32x16 (&acc)[BM / WGM / 32][BN / WGN / 32],
+                                              unsigned char* smem, int wave, int lane) {
+  using C = GemmCfg<BM, BN, WGM, WGN, STAGES>;
+  using E = Epilogue<EPI, C::WTN, C::CST>;
+  const int wm = wave / WGN, wn = wave - wm * WGN;
+  const int r32 = lane & 31, g = lane >> 5;
   float* const Cw = reinterpret_cast<float*>(smem) + wave * 32 * C::CST;
-  const int mw0 = m0 + wm * C::WTM;
+  const int mw0 = m0 + wm * C::WTM, nw0 = n0 + wn * C::WTN;
   f32x4 xcur[E::NX], xnext[E::NX];
   epi.load_resid(xcur, P, mw0, nw0, lane);
   __syncthreads();
@@ -402,6 +406,37 @@ __global__ __launch_bounds__(WGM * WGN * 64) void gemm_bf16_kernel(GemmArgs args
 #pragma unroll
     for (int t = 0; t < E::NX; ++t) xcur[t] = xnext[t];
   }
+}
+
+// One tile per workgroup.
+template <int BM, int BN, int WGM, int WGN, int STAGES, int EPI>
+__global__ __launch_bounds__(WGM * WGN * 64) void gemm_bf16_kernel(GemmArgs args) {
+  using C = GemmCfg<BM, BN, WGM, WGN, STAGES>;
+  __shared__ __attribute__((aligned(1024))) unsigned char smem[C::LDS];
+
+  const int tile = xcd_remap(blockIdx.x, args.total_tiles);
+  // Select the problem by value: indexing the by-value argument array with a
+  // runtime index would copy it to scratch memory.
+  const bool second = args.nprob > 1 && tile >= args.p[1].tile_begin;
+  const GemmProb P = second ? args.p[1] : args.p[0];
+  int m0, n0;
+  tile_origin<BM, BN>(P, tile - P.tile_begin, m0, n0);
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform (scalar) index
+  const int wm = wave / WGN, wn = wave - wm * WGN;
+  const unsigned lds0 = __builtin_amdgcn_readfirstlane(lds_address(smem));
+
+  // Epilogue constants (bias, gate) are requested first, so they are resident
+  // long before the epilogue; being older than every DMA, they never delay
+  // the explicit vmcnt waits of the main loop.
+  using E = Epilogue<EPI, C::WTN, C::CST>;
+  const bool vcols = EPI == EPI_QKV && n0 >= 2 * P.hidden;  // tiles never straddle k|v (2D % BN == 0)
+  E epi;
+  epi.init(P, n0 + wn * C::WTN, m0 + wm * C::WTM, vcols, lane);
+
+  f32x16 acc[C::TM][C::TN];
+  gemm_mainloop<BM, BN, WGM, WGN, STAGES>(P, m0, n0, 0, P.K / C::BK, acc, smem, lds0, wave, lane);
+  gemm_epilogue<BM, BN, WGM, WGN, STAGES, EPI>(P, m0, n0, vcols, epi, acc, smem, wave, lane);
 }
 
 // ---------------------------------------------------------------- 64 x 144 tiles

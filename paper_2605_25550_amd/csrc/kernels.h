@@ -35,7 +35,8 @@ struct GemmProb {
   void* k;             // [B, H, Tj, qk_stride]
   void* v;             // bf16: v^T [B, H, dh, Tj_pad], key j at column v_key_pos(j); fp32: [B, H, Tj, dh]
   int seq_off, Tj, Tj_pad, heads, head_dim, hidden;
-  int qk_stride;       // q/k row length: head_dim, or (bf16) head_dim rounded up to 16, zero padded
+  int qk_stride;       // q/k row length: head_dim, or (bf16) head_dim rounded up to 16, padded with
+                       // zeros except k's column head_dim, which holds 1
   float k_scale;       // bf16: k is stored multiplied by this (log2(e)/sqrt(dh), the softmax's exp2 scale)
 };
 
@@ -55,7 +56,7 @@ __host__ __device__ __forceinline__ int v_key_pos(int j) { return (j & ~12) | ((
 // ------------------------------------------------------------------ attention
 struct AttnArgs {
   const void* q;   // bf16: [B, H, Tj, round16(dh)] zero padded; fp32: [B, H, Tj, dh]
-  const void* k;   // same layout as q
+  const void* k;   // same layout as q; bf16 with padding: column dh holds 1
   const void* v;   // bf16: v^T [B, H, dh, Tj_pad] (key j at column v_key_pos(j)); fp32: [B, H, Tj, dh]
   void* o;         // stream-major rows: image b*T + t, then text B*T + b*Tt + t; [*, H*dh]
   int B, H, Tj, Tj_pad, T_img, T_txt, D;
