@@ -179,41 +179,52 @@ struct Gemm {
 };
 
 // bf16 tile choice, from per-shape measurements on MI355X (256 CUs).
-// Per CU, 256 x 256 tiles (eight waves, one workgroup per CU) are the most
-// efficient: a CU then fetches (BM + BN) / (BM BN) = 1/128 of the bytes per
-// flop that 128 x 128 tiles need, and its LDS reads per flop are a third
-// lower.  They cost a whole round of 256 tiles each, so they are used when
-// the tiles fill one round well (129..256 tiles) or when there are many
-// rounds and 256 x 128 tiles would not save a round.  Below one round of
-// 256 x 256, 256 x 128 tiles are used if there are at least 128 of them.  N
-// a multiple of 144 with 193..256 tiles of 64 x 144 (DiT-XL/2 at 256 tokens
-// x 8: the output projection and fc2) gets one balanced round of those.
-// Otherwise (small problems, or 257..511 tiles of 256 x 256) the 128 x 128 /
+// Per CU, the 256-row tiles (eight waves, one workgroup per CU) are the most
+// efficient: a CU fetches (BM + BN) / (BM BN) bytes per flop, 1/128 for
+// 256 x 256 against 1/64 for 128 x 128, and its LDS reads per flop are lower
+// too.  Among 256 x 256, 256 x 192 and 256 x 128 the estimate
+//   rounds of 256 tiles x BM x BN / efficiency
+// decides, with relative per-CU efficiencies 1, 0.97 and 0.87 measured on
+// the DiT shapes (ties go to the larger tile).  256 x 192 is not used
+// with the residual epilogue (it would spill registers).  N a multiple of
+// 144 with 193..256 tiles of 64 x 144 (DiT-XL/2 at 256 tokens x 8: the
+// output projection and fc2) gets one balanced round of those first.
+// Problems with fewer than 128 tiles of 256 x 128 use the 128 x 128 /
 // 64 x 128 rules: 128 x 128 (two workgroups per CU) for 256..511 and >= 768
 // tiles of 128 x 128, 64 x 128 with a 2-slot ring (three per CU) for
 // 512..767, and 64 x 128 with a 3-slot ring below 256.
 // The QKV epilogue needs tiles that do not straddle the k | v boundary at
 // column 2D, i.e. BN dividing 2D.
+static double tile_rounds(long tiles) { return (double)((tiles + 255) / 256); }
+
 int choose_tile(const GemmProb* p, int np, int epi) {
-  long t128 = 0, t144 = 0, t256 = 0, t2x1 = 0;
-  bool n144 = true, ok256 = true, ok128 = true;
+  long t128 = 0, t144 = 0, t256 = 0, t2x1 = 0, t192 = 0;
+  bool n144 = true, ok256 = true, ok128 = true, ok192 = epi != EPI_RESID && epi != EPI_RESID2;
   for (int i = 0; i < np; ++i) {
     const long M = p[i].M, N = p[i].N;
     t128 += ((M + 127) / 128) * ((N + 127) / 128);
     t144 += ((M + 63) / 64) * (N / 144);
     t256 += ((M + 255) / 256) * ((N + 255) / 256);
     t2x1 += ((M + 255) / 256) * ((N + 127) / 128);
+    t192 += ((M + 255) / 256) * ((N + 191) / 192);
     n144 = n144 && N % 144 == 0 && (epi != EPI_QKV || (2 * p[i].hidden) % 144 == 0);
     ok256 = ok256 && (epi != EPI_QKV || (2 * p[i].hidden) % 256 == 0);
+    ok192 = ok192 && (epi != EPI_QKV || (2 * p[i].hidden) % 192 == 0);
     ok128 = ok128 && (epi != EPI_QKV || (2 * p[i].hidden) % 128 == 0);
   }
   if (n144 && t144 > 192 && t144 <= 256) return TILE_64x144;
-  if (ok256 && t256 > 128 && t256 <= 256) return TILE_256x256;
-  if (ok256 && t256 >= 512) {
-    const long r256 = (t256 + 255) / 256, r2x1 = (t2x1 + 255) / 256;  // 256 x 128 rounds take half as long
-    return ok128 && r2x1 < 2 * r256 ? TILE_256x128 : TILE_256x256;
+  if (t2x1 >= 128) {
+    int best = -1;
+    double best_cost = 0.0;
+    auto consider = [&](bool ok, int cfg, long tiles, double area_over_eff) {
+      const double c = tile_rounds(tiles) * area_over_eff;
+      if (ok && (best < 0 || c < best_cost)) best = cfg, best_cost = c;
+    };
+    consider(ok256, TILE_256x256, t256, 256.0 * 256.0 / 1.0);
+    consider(ok192, TILE_256x192, t192, 256.0 * 192.0 / 0.97);
+    consider(ok128, TILE_256x128, t2x1, 256.0 * 128.0 / 0.87);
+    if (best >= 0) return best;
   }
-  if (ok128 && t256 <= 128 && t2x1 >= 128) return TILE_256x128;
   if ((t128 >= 256 && t128 < 512) || t128 >= 768) return TILE_128x128;
   if (t128 >= 512) return TILE_64x128_S2;
   return TILE_64x128;

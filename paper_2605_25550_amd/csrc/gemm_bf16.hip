@@ -624,6 +624,7 @@ void gemm_tile_dims(int tile_cfg, int* bm, int* bn) {
     case TILE_64x144: *bm = 64; *bn = 144; break;
     case TILE_256x256: *bm = 256; *bn = 256; break;
     case TILE_256x128: *bm = 256; *bn = 128; break;
+    case TILE_256x192: *bm = 256; *bn = 192; break;
     default: *bm = 64; *bn = 128; break;
   }
 }
@@ -667,6 +668,7 @@ hipError_t launch_gemm_bf16(const GemmArgs& a, int epi, int tile_cfg, hipStream_
     case TILE_64x144: return launch_144(a, epi, st);
     case TILE_256x256: return launch_tile<256, 256, 2, 4, 2>(a, epi, st);
     case TILE_256x128: return launch_tile<256, 128, 4, 2, 3>(a, epi, st);
+    case TILE_256x192: return launch_tile<256, 192, 4, 2, 2>(a, epi, st);
     default: return launch_tile<128, 128, 2, 2, 2>(a, epi, st);
   }
 }

@@ -117,7 +117,7 @@ hipError_t launch_axpy_f32(float* z, const float* v, float a, long n, hipStream_
 // Tile configurations of the bf16 GEMM (BM x BN, LDS ring depth).
 enum {
   TILE_128x128 = 0, TILE_64x128 = 1, TILE_64x128_S2 = 2, TILE_64x144 = 3,
-  TILE_256x256 = 4, TILE_256x128 = 5, TILE_COUNT = 6
+  TILE_256x256 = 4, TILE_256x128 = 5, TILE_256x192 = 6, TILE_COUNT = 7
 };
 void gemm_tile_dims(int tile_cfg, int* bm, int* bn);
 
