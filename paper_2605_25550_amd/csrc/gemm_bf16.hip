@@ -449,27 +449,34 @@ __global__ __launch_bounds__(WGM * WGN * 64) void gemm_bf16_kernel(GemmArgs args
 // 8*(lane/16) + 32*step; D: column lane%16, rows 4*(lane/16) + i).  Same
 // slice format, swizzle, DMA ring and refill rule as the kernel above; the
 // slice's 26 DMA instructions are spread 5 per wave, and the 4 spare ones
-// re-read a valid row into a dummy LDS line.  The ring (3 x 26 KB) lets two
+// re-read a valid row into a dummy LDS line.  Six waves leave two SIMDs with
+// two waves and two with one, so with KG = 2 the workgroup holds two such
+// k-groups of six waves (three waves per SIMD), each with its own ring of
+// 3 x 26 KB, taking alternate k-slices; at the end k-group 1 hands its
+// partial sums to k-group 0 through LDS.  With KG = 1 the ring lets two
 // workgroups share a CU.
+template <int KG>
 struct Gemm144 {
-  static constexpr int BM = 64, BN = 144, BK = 64, STAGES = 3, NW = 6;
+  static constexpr int BM = 64, BN = 144, BK = 64, STAGES = 3, NW = 6;  // per k-group
   static constexpr int ROWS = BM + BN;                // 208
   static constexpr int SLICE = ROWS * 128;            // bytes per slice buffer
   static constexpr int NDMA = ROWS / 8;               // 26 DMA instructions per slice
   static constexpr int IPW = (NDMA + NW - 1) / NW;    // 5 per wave
   static constexpr int TM = 2, TN = 3, WTM = 32, WTN = 48;
   static constexpr int CST = WTN + 4;                 // fp32 row stride of an epilogue slab
-  static constexpr int SPARE = STAGES * SLICE;        // dummy target of the spare DMAs
+  static constexpr int SPARE = KG * STAGES * SLICE;   // dummy target of the spare DMAs
   static constexpr int LDS_MAIN = SPARE + 1024;
   static constexpr int LDS_EPI = NW * 32 * CST * 4;
   static constexpr int LDS = LDS_MAIN > LDS_EPI ? LDS_MAIN : LDS_EPI;
   static_assert((STAGES - 1) * IPW < 64, "vmcnt range");
-  static_assert(2 * LDS <= 160 * 1024, "two workgroups per CU");
+  static_assert(KG == 2 || 2 * LDS <= 160 * 1024, "two workgroups per CU");
+  static_assert(LDS <= 160 * 1024, "LDS per CU");
+  static_assert(TM * TN * 4 * 64 <= 32 * CST, "a k-group's partial fits the wave's epilogue region");
 };
 
-template <int EPI>
-__global__ __launch_bounds__(384) void gemm_bf16_144_kernel(GemmArgs args) {
-  using C = Gemm144;
+template <int EPI, int KG>
+__global__ __launch_bounds__(384 * KG) void gemm_bf16_144_kernel(GemmArgs args) {
+  using C = Gemm144<KG>;
   __shared__ __attribute__((aligned(1024))) unsigned char smem[C::LDS];
 
   const int tile = xcd_remap(blockIdx.x, args.total_tiles);
@@ -485,15 +492,17 @@ __global__ __launch_bounds__(384) void gemm_bf16_144_kernel(GemmArgs args) {
   const int m0 = (first_m + in_group % gm) * C::BM;
   const int n0 = (in_group / gm) * C::BN;
 
-  const bf16_t* __restrict__ A = (const bf16_t*)P.A;
-  const bf16_t* __restrict__ W = (const bf16_t*)P.W;
-  const int M = P.M, N = P.N, K = P.K;
-  const int KT = K / C::BK;
   const int tid = threadIdx.x, lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wave_id = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int kg = wave_id / C::NW;                 // k-group: slices kg, kg + KG, kg + 2 KG, ...
+  const int wave = wave_id - kg * C::NW;          // wave within the k-group
+  const bf16_t* __restrict__ A = (const bf16_t*)P.A + kg * C::BK;
+  const bf16_t* __restrict__ W = (const bf16_t*)P.W + kg * C::BK;
+  const int M = P.M, N = P.N, K = P.K;
+  const int KT = K / (C::BK * KG);                // slices per k-group (K / 64 is a multiple of KG)
   const int wm = wave / 3, wn = wave - 3 * wm;
   const int r16 = lane & 15, g4 = lane >> 4;
-  const unsigned lds0 = __builtin_amdgcn_readfirstlane(lds_address(smem));
+  const unsigned lds0 = __builtin_amdgcn_readfirstlane(lds_address(smem)) + (unsigned)(kg * C::STAGES * C::SLICE);
 
   // DMA instruction t of this wave fills slice rows 8q .. 8q+7, q = wave + 6t
   // (A rows for q < 8, W rows for q < 26, spare above); lane -> row 8q +
@@ -509,8 +518,9 @@ __global__ __launch_bounds__(384) void gemm_bf16_144_kernel(GemmArgs args) {
   }
   auto dma_one = [&](int slice, int slot, int t) {
     const int q = wave + C::NW * t;  // wave-uniform
-    const unsigned dst = q < C::NDMA ? lds0 + (unsigned)(slot * C::SLICE + q * 1024) : lds0 + (unsigned)C::SPARE;
-    dma_16s((q < C::BM / 8 || q >= C::NDMA ? A : W) + (long)slice * C::BK, voff[t], dst);
+    const unsigned dst = q < C::NDMA ? lds0 + (unsigned)(slot * C::SLICE + q * 1024)
+                                     : lds0 - (unsigned)(kg * C::STAGES * C::SLICE) + (unsigned)C::SPARE;
+    dma_16s((q < C::BM / 8 || q >= C::NDMA ? A : W) + (long)slice * (KG * C::BK), voff[t], dst);
   };
   auto issue = [&](int slice, int slot) {
 #pragma unroll
@@ -543,7 +553,7 @@ __global__ __launch_bounds__(384) void gemm_bf16_144_kernel(GemmArgs args) {
   bf16x8 xa[C::TM], xb[C::TN], ya[C::TM], yb[C::TN];
 #define G144_READ(FA, FB, slot, s)                                                            \
   do {                                                                                       \
-    const unsigned char* b_ = smem + (slot) * C::SLICE;                                      \
+    const unsigned char* b_ = smem + (kg * C::STAGES + (slot)) * C::SLICE;                   \
     _Pragma("unroll") for (int i = 0; i < C::TM; ++i) FA[i] = *(const bf16x8*)(b_ + a_off[s][i]); \
     _Pragma("unroll") for (int j = 0; j < C::TN; ++j) FB[j] = *(const bf16x8*)(b_ + b_off[s][j]); \
   } while (0)
@@ -571,7 +581,7 @@ __global__ __launch_bounds__(384) void gemm_bf16_144_kernel(GemmArgs args) {
   const int mw0 = m0 + wm * C::WTM, nw0 = n0 + wn * C::WTN;
   const bool vcols = EPI == EPI_QKV && n0 >= 2 * P.hidden;  // the host only picks 144 when 2D % 144 == 0
   E epi;
-  epi.init(P, nw0, mw0, vcols, lane);
+  if (kg == 0) epi.init(P, nw0, mw0, vcols, lane);
 
 #pragma unroll
   for (int s = 0; s < C::STAGES; ++s)
@@ -606,8 +616,30 @@ __global__ __launch_bounds__(384) void gemm_bf16_144_kernel(GemmArgs args) {
   // epilogue: each wave stages its 32 x 48 accumulators in its own LDS region
   float* const Cw = reinterpret_cast<float*>(smem) + wave * 32 * C::CST;
   f32x4 xr[E::NX];
-  epi.load_resid(xr, P, mw0, nw0, lane);
-  __syncthreads();
+  if (kg == 0) epi.load_resid(xr, P, mw0, nw0, lane);
+  __syncthreads();  // every wave is done with the slice ring
+  if (KG == 2) {
+    // k-group 1 hands its partial sums to the wave of k-group 0 that owns
+    // the same outputs, through that wave's epilogue region (lane-major),
+    // and leaves; that wave adds them before staging its own.
+    if (kg == 1) {
+#pragma unroll
+      for (int i = 0; i < C::TM; ++i)
+#pragma unroll
+        for (int j = 0; j < C::TN; ++j)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) Cw[((i * C::TN + j) * 4 + e) * 64 + lane] = acc[i][j][e];
+    }
+    __syncthreads();
+    if (kg == 1) return;
+#pragma unroll
+    for (int i = 0; i < C::TM; ++i)
+#pragma unroll
+      for (int j = 0; j < C::TN; ++j)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) acc[i][j][e] += Cw[((i * C::TN + j) * 4 + e) * 64 + lane];
+    wave_lds_fence();  // the partial is read before the region is overwritten
+  }
 #pragma unroll
   for (int i = 0; i < C::TM; ++i)
 #pragma unroll
@@ -629,16 +661,25 @@ void gemm_tile_dims(int tile_cfg, int* bm, int* bn) {
   }
 }
 
-static hipError_t launch_144(const GemmArgs& a, int epi, hipStream_t st) {
-  dim3 grid(a.total_tiles), block(Gemm144::NW * 64);
+template <int KG>
+static hipError_t launch_144_kg(const GemmArgs& a, int epi, hipStream_t st) {
+  dim3 grid(a.total_tiles), block(Gemm144<KG>::NW * KG * 64);
   switch (epi) {
-    case EPI_QKV: hipLaunchKernelGGL((gemm_bf16_144_kernel<EPI_QKV>), grid, block, 0, st, a); break;
-    case EPI_GELU: hipLaunchKernelGGL((gemm_bf16_144_kernel<EPI_GELU>), grid, block, 0, st, a); break;
-    case EPI_RESID: hipLaunchKernelGGL((gemm_bf16_144_kernel<EPI_RESID>), grid, block, 0, st, a); break;
-    case EPI_RESID2: hipLaunchKernelGGL((gemm_bf16_144_kernel<EPI_RESID2>), grid, block, 0, st, a); break;
-    default: hipLaunchKernelGGL((gemm_bf16_144_kernel<EPI_STORE>), grid, block, 0, st, a); break;
+    case EPI_QKV: hipLaunchKernelGGL((gemm_bf16_144_kernel<EPI_QKV, KG>), grid, block, 0, st, a); break;
+    case EPI_GELU: hipLaunchKernelGGL((gemm_bf16_144_kernel<EPI_GELU, KG>), grid, block, 0, st, a); break;
+    case EPI_RESID: hipLaunchKernelGGL((gemm_bf16_144_kernel<EPI_RESID, KG>), grid, block, 0, st, a); break;
+    case EPI_RESID2: hipLaunchKernelGGL((gemm_bf16_144_kernel<EPI_RESID2, KG>), grid, block, 0, st, a); break;
+    default: hipLaunchKernelGGL((gemm_bf16_144_kernel<EPI_STORE, KG>), grid, block, 0, st, a); break;
   }
   return hipGetLastError();
+}
+
+// Two k-groups (twelve waves, three per SIMD) where every problem has an
+// even number of k-slices; one group of six waves otherwise.
+static hipError_t launch_144(const GemmArgs& a, int epi, hipStream_t st) {
+  bool even = true;
+  for (int i = 0; i < a.nprob; ++i) even = even && (a.p[i].K / 64) % 2 == 0;
+  return even ? launch_144_kg<2>(a, epi, st) : launch_144_kg<1>(a, epi, st);
 }
 
 template <int BM, int BN, int WGM, int WGN, int STAGES>
