@@ -33,14 +33,20 @@ PROFILES = os.path.join(ROOT, "profiles")
 # GEMM classes differ in the last template argument (the fused epilogue), for
 # both GEMM kernels (gemm_bf16_kernel<BM, BN, WGM, WGN, STAGES, EPI>,
 # gemm_bf16_144_kernel<EPI>).
+def _gemm_re(epi: int) -> str:
+    # generic kernel: epilogue is the last of six template arguments; the
+    # 64x144 kernel: <epilogue, k-groups>
+    return rf"gemm_bf16_(?:kernel<(?:\d+, ){{5}}{epi}>|144_kernel<{epi}, \d+>)"
+
+
 CLASSES = {
-    "gemm_qkv": (r"gemm_bf16_\w*kernel<(?:\d+, )*0>", "gemm_bf16.hip"),
+    "gemm_qkv": (_gemm_re(0), "gemm_bf16.hip"),
     "attention": (r"attn_bf16_\w*kernel<", "attention_bf16.hip"),
-    "gemm_out": (r"gemm_bf16_\w*kernel<(?:\d+, )*2>", "gemm_bf16.hip"),
-    "gemm_fc1": (r"gemm_bf16_\w*kernel<(?:\d+, )*1>", "gemm_bf16.hip"),
-    "gemm_fc2": (r"gemm_bf16_\w*kernel<(?:\d+, )*4>", "gemm_bf16.hip"),
+    "gemm_out": (_gemm_re(2), "gemm_bf16.hip"),
+    "gemm_fc1": (_gemm_re(1), "gemm_bf16.hip"),
+    "gemm_fc2": (_gemm_re(4), "gemm_bf16.hip"),
     "ln_mod": (r"ln_mod_kernel<", "elementwise.hip"),
-    "adaln": (r"adaln_kernel<", "elementwise.hip"),
+    "adaln": (r"adaln\w*_kernel", "elementwise.hip"),
 }
 
 

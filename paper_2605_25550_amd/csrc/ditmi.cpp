@@ -186,7 +186,9 @@ struct Gemm {
 //   rounds of 256 tiles x BM x BN / efficiency
 // decides, with relative per-CU efficiencies 1, 0.97 and 0.87 measured on
 // the DiT shapes (ties go to the larger tile).  256 x 192 is not used
-// with the residual epilogue (it would spill registers).  N a multiple of
+// with the residual epilogue (it would spill registers), nor beyond two
+// rounds (measured slower there, e.g. the joint DiT's fc1 at 4352 rows:
+// 8.48 ms per step against 7.86 ms with 256 x 256).  N a multiple of
 // 144 with 193..256 tiles of 64 x 144 (DiT-XL/2 at 256 tokens x 8: the
 // output projection and fc2) gets one balanced round of those first.
 // Problems with fewer than 128 tiles of 256 x 128 use the 128 x 128 /
@@ -221,7 +223,7 @@ int choose_tile(const GemmProb* p, int np, int epi) {
       if (ok && (best < 0 || c < best_cost)) best = cfg, best_cost = c;
     };
     consider(ok256, TILE_256x256, t256, 256.0 * 256.0 / 1.0);
-    consider(ok192, TILE_256x192, t192, 256.0 * 192.0 / 0.97);
+    consider(ok192 && t192 <= 512, TILE_256x192, t192, 256.0 * 192.0 / 0.97);
     consider(ok128, TILE_256x128, t2x1, 256.0 * 128.0 / 0.87);
     if (best >= 0) return best;
   }
