@@ -76,6 +76,7 @@ struct AttnCfg {
 template <int DH, int NW, int QT>
 __global__ __launch_bounds__(NW * 64, QT == 1 ? 8 / NW : 1) void attn_bf16_dma_kernel(AttnArgs a) {
   using C = AttnCfg<DH>;
+  constexpr bool FOLD = C::FOLD;  // softmax bookkeeping in the MFMAs, as in the pipelined kernel below
   constexpr int IPW = (C::TDMA + NW - 1) / NW;  // DMA instructions per wave per tile (uniform)
   // ring of slots, then a 1 KB line that absorbs the spare DMAs
   __shared__ __attribute__((aligned(1024))) unsigned char smem[C::STAGES * C::SLOT + 1024];
@@ -121,11 +122,12 @@ __global__ __launch_bounds__(NW * 64, QT == 1 ? 8 / NW : 1) void attn_bf16_dma_k
   };
 
   // V^T rows past head_dim (head_dim 72 only) are never written by the DMA
-  // and feed discarded O^T rows; keep them zero in every slot.
+  // and feed discarded O^T rows: zero in every slot, except row DH, all
+  // ones with FOLD (O^T row DH = the row sum l).
   if (C::VROWS > DH) {
     for (int e = tid; e < C::STAGES * (C::VROWS - DH) * 32; e += NW * 64) {
       const int sl = e / ((C::VROWS - DH) * 32), w = e % ((C::VROWS - DH) * 32);
-      ((uint32_t*)(smem + sl * C::SLOT + C::KTILE + DH * 128))[w] = 0u;
+      ((uint32_t*)(smem + sl * C::SLOT + C::KTILE + DH * 128))[w] = FOLD && w < 32 ? 0x3F803F80u : 0u;
     }
   }
 
@@ -154,14 +156,16 @@ __global__ __launch_bounds__(NW * 64, QT == 1 ? 8 / NW : 1) void attn_bf16_dma_k
   const float sc = a.scale_log2;
   // Lazy max: probabilities are exp2(s*scale - m_run) <= 2^TAU; bf16 and fp32
   // hold 2^64 exactly in range, and O^T / l sums stay far from fp32 overflow.
+  // With FOLD the product already subtracts m_run (0 before the first tile).
   const float TAU = 64.0f;
   float m_run[QT], l_run[QT];
   f32x16 oacc[QT][C::DT];
 #pragma unroll
   for (int qt = 0; qt < QT; ++qt) {
-    m_run[qt] = -INFINITY;
+    m_run[qt] = FOLD ? 0.f : -INFINITY;
     l_run[qt] = 0.f;
   }
+  bool first = true;
 #pragma unroll
   for (int qt = 0; qt < QT; ++qt)
 #pragma unroll
@@ -228,6 +232,26 @@ __global__ __launch_bounds__(NW * 64, QT == 1 ? 8 / NW : 1) void attn_bf16_dma_k
         for (int e = 0; e < 16; ++e) {
           mloc = fmaxf(mloc, sacc[qt][kt][e]);
         }
+      if (FOLD) {
+        // scores are relative to m_run already; the running max moves as in
+        // the pipelined kernel, kept exactly representable in bf16
+        mloc = max_halves(mloc);
+        if (first || __builtin_amdgcn_ballot_w64(mloc > TAU) != 0) {
+          const float m_new = bf2f(f2bf(m_run[qt] + (first ? mloc : fmaxf(mloc, 0.f))));
+          const float delta = m_new - m_run[qt];
+          const float alpha = __builtin_amdgcn_exp2f(-delta);
+#pragma unroll
+          for (int t = 0; t < C::DT; ++t) oacc[qt][t] *= alpha;
+#pragma unroll
+          for (int kt = 0; kt < 2; ++kt) sacc[qt][kt] -= delta;
+          m_run[qt] = m_new;
+          if (g == C::QG) qf[qt][C::QS][C::QE] = __builtin_bit_cast(__bf16, f2bf(-m_new));
+        }
+#pragma unroll
+        for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+          for (int e = 0; e < 16; ++e) sacc[qt][kt][e] = __builtin_amdgcn_exp2f(sacc[qt][kt][e]);
+      } else {
       mloc = max_halves(mloc) * sc;
       if (m_run[qt] == -INFINITY) {
         m_run[qt] = mloc;  // first tile: O and l are still zero, nothing to rescale
@@ -251,6 +275,7 @@ __global__ __launch_bounds__(NW * 64, QT == 1 ? 8 / NW : 1) void attn_bf16_dma_k
           lsum += p;
         }
       l_run[qt] += lsum;
+      }
 #pragma unroll
       for (int c = 0; c < 4; ++c) {
         const int kt = c >> 1, jb = (c & 1) * 2;
@@ -269,13 +294,14 @@ __global__ __launch_bounds__(NW * 64, QT == 1 ? 8 / NW : 1) void attn_bf16_dma_k
                                                                  __builtin_bit_cast(bf16x8, pw[qt][c]), oacc[qt][t], 0, 0, 0);
         }
     }
+    first = false;
   }
   wait_vmcnt<0>();
 
 #pragma unroll
   for (int qt = 0; qt < QT; ++qt) {
     const int qrow = q0 + qt * 32 + r32;
-    const float l_tot = sum_halves(l_run[qt]);
+    const float l_tot = sum_halves(FOLD ? (g == C::LG ? oacc[qt][C::LT][C::LE] : 0.f) : l_run[qt]);
     const float inv = 1.0f / l_tot;
     if (qrow < Tj) {
       const long orow = qrow < a.T_img ? (long)b * a.T_img + qrow
