@@ -446,7 +446,8 @@ dit_status run_adaln(const dit_shape* s, const float* cond, void* act, const std
       e.out = jobs[j].out;
       e.N = jobs[j].N;
       e.wg_begin = wg;
-      wg += (jobs[j].N + 127) / 128;
+      const int rows_per_wg = s->dtype == DIT_BF16 ? ADA_ROWS_PER_WG : 128;
+      wg += (jobs[j].N + rows_per_wg - 1) / rows_per_wg;
       bytes += (double)jobs[j].N * s->hidden * E;
     }
     a.total_wg = wg;

@@ -192,16 +192,20 @@ __global__ __launch_bounds__(256) void adaln_kernel(AdaArgs a) {
 }
 
 // bf16 weights: the same product on v_mfma_f32_16x16x32_bf16 as
-// out^T [N, B] = W [N, K] * SiLU(c)^T [K, B].  A workgroup (4 waves x 2 row
-// tiles of 16) owns 128 rows of one entry.  Both operands are read straight
-// from global memory, 16 bytes per lane (row lane%16, k offset 8*(lane/16)):
-// W streams from HBM once, and the B operand, SiLU(c) in bf16 for 16 samples
-// (computed once by silu_bf16_kernel, zero rows past the batch; at most a
-// few hundred KB), stays in L2.  No LDS, so many workgroups share a CU and
-// keep enough weight loads in flight to stream HBM (staging the B operand
-// in LDS held one workgroup per CU at hidden 3072).  Batches above 16 loop
-// over 16-sample tiles.  D lanes hold column (sample) lane%16, rows
-// 4*(lane/16) + i.
+// out^T [N, B] = W [N, K] * SiLU(c)^T [K, B].  A workgroup (4 waves x 4 row
+// tiles of 16) owns 256 rows of one entry; each B fragment feeds the four
+// row tiles.  Both operands are read straight from global memory, 16 bytes
+// per lane (row lane%16, k offset 8*(lane/16)): W streams from HBM once,
+// and the B operand, SiLU(c) in bf16 for 16 samples (computed once by
+// silu_bf16_kernel, zero rows past the batch; at most a few hundred KB),
+// stays in L2; lanes of samples past the batch supply zeros without a load
+// (at batch 1, fifteen of sixteen).  No LDS, so many workgroups share a CU
+// and keep enough weight loads in flight to stream HBM (staging the B
+// operand in LDS held one workgroup per CU at hidden 3072).  Measured:
+// 4.2 TB/s with two row tiles per wave and every lane loading, 4.7-5.2 TB/s
+// like this (a plain streaming read of the same rows: 5.8-6.1).  Batches
+// above 16 loop over 16-sample tiles.  D lanes hold column (sample)
+// lane%16, rows 4*(lane/16) + i.
 __global__ void silu_bf16_kernel(int B, int D, int rows, const float* cond, bf16_t* act) {
   const long idx = (long)blockIdx.x * blockDim.x + threadIdx.x;
   if (idx >= (long)rows * D) return;
@@ -218,38 +222,42 @@ hipError_t launch_silu_bf16(int B, int D, const float* cond, void* act, hipStrea
 }
 
 __global__ __launch_bounds__(256) void adaln_mfma_kernel(AdaArgs a) {
+  constexpr int RT = ADA_ROWS_PER_WG / 64;  // row tiles of 16 per wave
   const int wg = blockIdx.x;
   int ei = 0;
   while (ei + 1 < a.ne && wg >= a.e[ei + 1].wg_begin) ++ei;
   const AdaEntry& E = a.e[ei];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int K = a.D, N = E.N;
-  const int nbase = (wg - E.wg_begin) * 128 + wave * 32;
+  const int nbase = (wg - E.wg_begin) * ADA_ROWS_PER_WG + wave * (16 * RT);
   const bf16_t* __restrict__ W = (const bf16_t*)E.W;
   const bf16_t* __restrict__ bias = (const bf16_t*)E.bias;
   const bf16_t* __restrict__ act = (const bf16_t*)a.act;
   const int r16 = lane & 15, kq = lane >> 4;
-  const bf16_t* w0 = W + (long)min(nbase + r16, N - 1) * K + 8 * kq;
-  const bf16_t* w1 = W + (long)min(nbase + 16 + r16, N - 1) * K + 8 * kq;
+  const bf16_t* wr[RT];
+#pragma unroll
+  for (int t = 0; t < RT; ++t) wr[t] = W + (long)min(nbase + 16 * t + r16, N - 1) * K + 8 * kq;
 
   for (int b0 = 0; b0 < a.B; b0 += 16) {
+    const bool live = b0 + r16 < a.B;  // this lane's sample exists
     const bf16_t* sp = act + (long)(b0 + r16) * K + 8 * kq;
-    f32x4 acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
+    f32x4 acc[RT];
+#pragma unroll
+    for (int t = 0; t < RT; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll 8
     for (int k0 = 0; k0 < K; k0 += 32) {
-      const bf16x8 a0 = *(const bf16x8*)(w0 + k0);
-      const bf16x8 a1 = *(const bf16x8*)(w1 + k0);
-      const bf16x8 bv = *(const bf16x8*)(sp + k0);
-      acc0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0, bv, acc0, 0, 0, 0);
-      acc1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1, bv, acc1, 0, 0, 0);
+      const bf16x8 bv = live ? *(const bf16x8*)(sp + k0) : bf16x8{};
+#pragma unroll
+      for (int t = 0; t < RT; ++t)
+        acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(*(const bf16x8*)(wr[t] + k0), bv, acc[t], 0, 0, 0);
     }
     const int b = b0 + r16;
     if (b < a.B) {
 #pragma unroll
-      for (int t = 0; t < 2; ++t) {
+      for (int t = 0; t < RT; ++t) {
         const int n = nbase + 16 * t + 4 * kq;  // N is a multiple of 4
         if (n >= N) continue;
-        const f32x4 v = t ? acc1 : acc0;
+        const f32x4 v = acc[t];
         *(f32x4*)(E.out + (long)b * N + n) =
             f32x4{v[0] + bf2f(bias[n]), v[1] + bf2f(bias[n + 1]), v[2] + bf2f(bias[n + 2]), v[3] + bf2f(bias[n + 3])};
       }

@@ -80,6 +80,7 @@ struct LnArgs {
 
 // ------------------------------------------------------------------ adaLN GEMV
 constexpr int ADA_MAX_ENTRIES = 64;
+constexpr int ADA_ROWS_PER_WG = 256;  // bf16 MFMA kernel: output rows per workgroup (the fp32 kernel: 128)
 struct AdaEntry {
   const void* W;     // [N, D]
   const void* bias;  // [N]
