@@ -230,8 +230,9 @@ dit_status dit_pos_embed_2d(int32_t grid_h, int32_t grid_w, int32_t hidden, floa
 
 /* Kernel timing hook for measurement.  dit_timing_enable() (host allocation
  * of HIP events, not a compute call) makes every later launch of kernel class
- * `kclass` record a start/stop hipEvent pair on its launch stream, for up to
- * max_launches launches, and accumulates the algorithmic flops and bytes of
+ * `kclass` record a start/stop hipEvent pair on its launch stream (timing-only
+ * events, created without the system-scope fence), for up to max_launches
+ * launches, and accumulates the algorithmic flops and bytes of
  * those launches.  dit_timing_read() synchronises on the recorded events and
  * returns the sum of launch durations (ms), the number of launches, and the
  * algorithmic flop and byte totals.  dit_timing_disable() frees the events. */

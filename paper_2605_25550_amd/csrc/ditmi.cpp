@@ -176,6 +176,8 @@ struct Gemm {
   int epi = EPI_STORE;
   int kclass = DIT_K_OTHER;
   double flops = 0, bytes = 0;
+  float* part = nullptr;  // fp32 scratch for a split second problem (EPI_GELU), part_cap bytes
+  size_t part_cap = 0;
 };
 
 // bf16 tile choice, from per-shape measurements on MI355X (256 CUs).
@@ -199,7 +201,31 @@ struct Gemm {
 // column 2D, i.e. BN dividing 2D.
 static double tile_rounds(long tiles) { return (double)((tiles + 255) / 256); }
 
-int choose_tile(const GemmProb* p, int np, int epi) {
+// Tail schedule: where problem 0 fills whole rounds of 256 tiles and the few
+// tiles of problem 1 would take a round of their own (the joint block's fc1:
+// 768 image + 48 text tiles of 256 x 256), problem 1 is split into S equal
+// k-ranges (each at least 4 slices) whose S-times-shorter units fill that
+// round, and a reduction adds the ranges.  Returns S, or 0 for no split.
+static int tail_split(const GemmProb* p, int np, int epi, int bm, int bn, size_t part_cap) {
+  if (np != 2 || epi != EPI_GELU || part_cap == 0) return 0;
+  const long t0 = (long)((p[0].M + bm - 1) / bm) * ((p[0].N + bn - 1) / bn);
+  const long t1 = (long)((p[1].M + bm - 1) / bm) * ((p[1].N + bn - 1) / bn);
+  if (t0 < 256 || t0 % 256 != 0 || t1 == 0 || 2 * t1 > 256) return 0;
+  const int ks = p[1].K / 64;
+  for (int S = 8; S >= 2; --S)
+    if (t1 * S <= 256 && ks % S == 0 && ks / S >= 4 && (t1 * S) % 8 == 0 &&
+        (size_t)S * p[1].M * p[1].N * 4 <= part_cap)
+      return S;
+  return 0;
+}
+
+// Cost of the split tail in rounds: the short units plus their fixed costs
+// (prologue, fp32 partial stores, the reduction launch), estimated at 0.15
+// of a round.
+static double tail_rounds(long t0, int S) { return (double)(t0 / 256) + 1.0 / S + 0.15; }
+
+int choose_tile(const GemmProb* p, int np, int epi, size_t part_cap, int* split) {
+  *split = 0;
   long t128 = 0, t144 = 0, t256 = 0, t2x1 = 0, t192 = 0;
   bool n144 = true, ok256 = true, ok128 = true, ok192 = epi != EPI_RESID && epi != EPI_RESID2;
   for (int i = 0; i < np; ++i) {
@@ -216,16 +242,23 @@ int choose_tile(const GemmProb* p, int np, int epi) {
   }
   if (n144 && t144 > 192 && t144 <= 256) return TILE_64x144;
   if (t2x1 >= 128) {
-    int best = -1;
+    int best = -1, best_split = 0;
     double best_cost = 0.0;
     auto consider = [&](bool ok, int cfg, long tiles, double area_over_eff) {
-      const double c = tile_rounds(tiles) * area_over_eff;
-      if (ok && (best < 0 || c < best_cost)) best = cfg, best_cost = c;
+      int bm = 0, bn = 0;
+      gemm_tile_dims(cfg, &bm, &bn);
+      const int S = tail_split(p, np, epi, bm, bn, part_cap);
+      const long t0 = (long)((p[0].M + bm - 1) / bm) * ((p[0].N + bn - 1) / bn);
+      const double c = (S ? tail_rounds(t0, S) : tile_rounds(tiles)) * area_over_eff;
+      if (ok && (best < 0 || c < best_cost)) best = cfg, best_cost = c, best_split = S;
     };
     consider(ok256, TILE_256x256, t256, 256.0 * 256.0 / 1.0);
     consider(ok192 && t192 <= 512, TILE_256x192, t192, 256.0 * 192.0 / 0.97);
     consider(ok128, TILE_256x128, t2x1, 256.0 * 128.0 / 0.87);
-    if (best >= 0) return best;
+    if (best >= 0) {
+      *split = best_split;
+      return best;
+    }
   }
   if ((t128 >= 256 && t128 < 512) || t128 >= 768) return TILE_128x128;
   if (t128 >= 512) return TILE_64x128_S2;
@@ -234,9 +267,9 @@ int choose_tile(const GemmProb* p, int np, int epi) {
 
 hipError_t run_gemm(Gemm& G, int dtype, hipStream_t st) {
   GemmArgs& a = G.a;
-  int bm = 64, bn = 64, tcfg = 0;
+  int bm = 64, bn = 64, tcfg = 0, split = 0;
   if (dtype == DIT_BF16) {
-    tcfg = choose_tile(a.p, a.nprob, G.epi);
+    tcfg = choose_tile(a.p, a.nprob, G.epi, G.part_cap, &split);
     gemm_tile_dims(tcfg, &bm, &bn);
   }
   int tiles = 0;
@@ -245,12 +278,25 @@ hipError_t run_gemm(Gemm& G, int dtype, hipStream_t st) {
     p.tiles_m = (p.M + bm - 1) / bm;
     p.tiles_n = (p.N + bn - 1) / bn;
     p.tile_begin = tiles;
-    tiles += p.tiles_m * p.tiles_n;
+    p.ksplit = 0;
+    p.part = nullptr;
+    tiles += p.tiles_m * p.tiles_n * (i == 1 && split ? split : 1);
   }
   a.total_tiles = tiles;
+  a.tail = split ? 1 : 0;
+  if (split) {
+    a.p[1].ksplit = split;
+    a.p[1].part = G.part;
+  }
   if (tiles == 0) return hipSuccess;
-  return timed(G.kclass, G.flops, G.bytes, st, [&]() {
+  hipError_t e = timed(G.kclass, G.flops, G.bytes, st, [&]() {
     return dtype == DIT_BF16 ? launch_gemm_bf16(a, G.epi, tcfg, st) : launch_gemm_f32(a, G.epi, st);
+  });
+  if (e != hipSuccess || !split) return e;
+  const GemmProb& p1 = a.p[1];
+  const double mn = (double)p1.M * p1.N;
+  return timed(DIT_K_OTHER, 0, mn * (split * 4.0 + 2.0) + p1.N * 2.0, st, [&]() {
+    return launch_splitk_gelu_bf16(p1.part, split, p1.M, p1.N, p1.bias, p1.out, st);
   });
 }
 
@@ -393,6 +439,10 @@ dit_status run_block(const dit_shape* s, const Layout& L, char* ws, StreamIO* io
       prob_common(p, i, act(h, i, D), io[i].w->w_fc1, io[i].w->b_fc1, F, D);
       p.out = act(gbuf, i, F);
     }
+    // q, k and v are dead after attention: their region holds the fp32
+    // partials of a split text-stream problem.
+    G.part = (float*)(ws + L.q);
+    G.part_cap = L.o - L.q;
     G.flops = 2.0 * tokens * F * D;
     G.bytes = (tokens * D + ns * (double)F * D + tokens * F) * E;
     HIP_TRY(run_gemm(G, dt, st));
@@ -791,13 +841,16 @@ dit_status dit_timing_enable(int kclass, int max_launches) {
   dit_timing_disable();
   std::lock_guard<std::mutex> lk(g_timing.mu);
   g_timing.ev.assign(2 * (size_t)max_launches, nullptr);
+  // Timing-only events: without the system-scope fence an event record does
+  // not write back and invalidate the L2s, which would add several
+  // microseconds per record and slow the bracketed kernel's first accesses.
   for (auto& e : g_timing.ev) {
-    hipError_t r = hipEventCreate(&e);
+    hipError_t r = hipEventCreateWithFlags(&e, hipEventDisableSystemFence);
     if (r != hipSuccess) {
       for (auto& f : g_timing.ev)
         if (f) hipEventDestroy(f);
       g_timing.ev.clear();
-      return fail(DIT_ERR_HIP, "hipEventCreate: %s", hipGetErrorString(r));
+      return fail(DIT_ERR_HIP, "hipEventCreateWithFlags: %s", hipGetErrorString(r));
     }
   }
   g_timing.kclass = kclass;

@@ -189,6 +189,8 @@ struct Epilogue {
         xv[2] += g[2] * y2;
         xv[3] += g[3] * y3;
         *(f32x4*)(P.resid + (long)m * N + n) = xv;
+      } else if (EPI == EPI_GELU && P.ksplit > 1) {  // one k-range: raw fp32 partial (P.part at its range)
+        *(f32x4*)(P.part + (long)m * N + n) = y;
       } else if (EPI == EPI_GELU) {
         *(u32x2*)((bf16_t*)P.out + (long)m * N + n) =
             u32x2{pack_bf16x2(gelu_tanh(y0), gelu_tanh(y1)), pack_bf16x2(gelu_tanh(y2), gelu_tanh(y3))};
@@ -414,13 +416,30 @@ __global__ __launch_bounds__(WGM * WGN * 64) void gemm_bf16_kernel(GemmArgs args
   using C = GemmCfg<BM, BN, WGM, WGN, STAGES>;
   __shared__ __attribute__((aligned(1024))) unsigned char smem[C::LDS];
 
-  const int tile = xcd_remap(blockIdx.x, args.total_tiles);
+  int tile;
+  if (args.tail) {  // XCD x = blockIdx % 8 runs n0 tiles of problem 0, then n1 units of problem 1
+    const int n0 = args.p[1].tile_begin >> 3, n1 = (args.total_tiles - args.p[1].tile_begin) >> 3;
+    const int xcd = blockIdx.x & 7, idx = blockIdx.x >> 3;
+    tile = idx < n0 ? xcd * n0 + idx : args.p[1].tile_begin + xcd * n1 + (idx - n0);
+  } else {
+    tile = xcd_remap(blockIdx.x, args.total_tiles);
+  }
   // Select the problem by value: indexing the by-value argument array with a
   // runtime index would copy it to scratch memory.
   const bool second = args.nprob > 1 && tile >= args.p[1].tile_begin;
-  const GemmProb P = second ? args.p[1] : args.p[0];
+  GemmProb P = second ? args.p[1] : args.p[0];
+  // Split K: unit u of the problem is k-range u / (tiles_m tiles_n) of tile
+  // u % (tiles_m tiles_n).
+  int local = tile - P.tile_begin, kb = 0, nks = P.K / C::BK;
+  if (EPI == EPI_GELU && P.ksplit > 1) {
+    const int per = P.tiles_m * P.tiles_n, s = local / per;
+    local -= s * per;
+    nks /= P.ksplit;
+    kb = s * nks;
+    P.part += (long)s * P.M * P.N;
+  }
   int m0, n0;
-  tile_origin<BM, BN>(P, tile - P.tile_begin, m0, n0);
+  tile_origin<BM, BN>(P, local, m0, n0);
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform (scalar) index
   const int wm = wave / WGN, wn = wave - wm * WGN;
@@ -435,7 +454,7 @@ __global__ __launch_bounds__(WGM * WGN * 64) void gemm_bf16_kernel(GemmArgs args
   epi.init(P, n0 + wn * C::WTN, m0 + wm * C::WTM, vcols, lane);
 
   f32x16 acc[C::TM][C::TN];
-  gemm_mainloop<BM, BN, WGM, WGN, STAGES>(P, m0, n0, 0, P.K / C::BK, acc, smem, lds0, wave, lane);
+  gemm_mainloop<BM, BN, WGM, WGN, STAGES>(P, m0, n0, kb, nks, acc, smem, lds0, wave, lane);
   gemm_epilogue<BM, BN, WGM, WGN, STAGES, EPI>(P, m0, n0, vcols, epi, acc, smem, wave, lane);
 }
 
@@ -648,6 +667,38 @@ __global__ __launch_bounds__(384 * KG) void gemm_bf16_144_kernel(GemmArgs args) 
       for (int e = 0; e < 4; ++e) Cw[(i * 16 + 4 * g4 + e) * C::CST + j * 16 + r16] = acc[i][j][e];
   wave_lds_fence();  // own region only: the LDS runs a wave's accesses in order
   epi.apply(P, Cw, mw0, nw0, vcols, lane, xr);
+}
+
+// Split-K reduction: four consecutive outputs per lane, 16-byte loads of
+// each k-range's partial; bias, GELU and bf16 rounding as in the GEMM
+// epilogue.
+__global__ __launch_bounds__(256) void splitk_gelu_kernel(const float* __restrict__ part, int S, long MN, int N,
+                                                          const bf16_t* __restrict__ bias, bf16_t* __restrict__ out) {
+  const long e = (blockIdx.x * 256L + threadIdx.x) * 4;
+  if (e >= MN) return;
+  f32x4 y = *(const f32x4*)(part + e);
+  for (int s = 1; s < S; ++s) {
+    const f32x4 p = *(const f32x4*)(part + s * MN + e);
+    y[0] += p[0];
+    y[1] += p[1];
+    y[2] += p[2];
+    y[3] += p[3];
+  }
+  const int n = (int)(e % N);
+  const u32x2 w = *(const u32x2*)(bias + n);
+  const float y0 = y[0] + __uint_as_float(w[0] << 16), y1 = y[1] + __uint_as_float(w[0] & 0xFFFF0000u);
+  const float y2 = y[2] + __uint_as_float(w[1] << 16), y3 = y[3] + __uint_as_float(w[1] & 0xFFFF0000u);
+  *(u32x2*)(out + e) = u32x2{pack_bf16x2(gelu_tanh(y0), gelu_tanh(y1)), pack_bf16x2(gelu_tanh(y2), gelu_tanh(y3))};
+}
+
+hipError_t launch_splitk_gelu_bf16(const float* part, int S, int M, int N, const void* bias, void* out,
+                                   hipStream_t st) {
+  const long MN = (long)M * N;
+  if (MN == 0) return hipSuccess;
+  const long groups = MN / 4;
+  hipLaunchKernelGGL(splitk_gelu_kernel, dim3((unsigned)((groups + 255) / 256)), dim3(256), 0, st, part, S, MN, N,
+                     (const bf16_t*)bias, (bf16_t*)out);
+  return hipGetLastError();
 }
 
 void gemm_tile_dims(int tile_cfg, int* bm, int* bn) {

@@ -38,12 +38,23 @@ struct GemmProb {
   int qk_stride;       // q/k row length: head_dim, or (bf16) head_dim rounded up to 16, padded with
                        // zeros except k's column head_dim, which holds 1
   float k_scale;       // bf16: k is stored multiplied by this (log2(e)/sqrt(dh), the softmax's exp2 scale)
+  // Split K (bf16, EPI_GELU, second problem only): ksplit > 1 divides the
+  // k-slices into ksplit equal ranges; the unit of tile t and range s stores
+  // its fp32 product without bias to part[s][M][N], and
+  // launch_splitk_gelu_bf16 then adds the ranges, the bias and the GELU.
+  float* part;
+  int ksplit;
 };
 
 struct GemmArgs {
   GemmProb p[2];
   int nprob;
   int total_tiles;
+  // Tail schedule (set with p[1].ksplit > 1): the tile counts of both
+  // problems are multiples of 8, and every XCD runs its share of problem 0's
+  // tiles before its share of problem 1's units, so the short split units
+  // fill the last round instead of whole tiles.
+  int tail;
 };
 
 // Column of key j in a bf16 v^T row: within each group of 16 keys the
@@ -98,6 +109,10 @@ struct AdaArgs {
 // ------------------------------------------------------------------ launchers
 // Each returns hipSuccess or the launch error.  dtype: 0 = fp32, 1 = bf16.
 hipError_t launch_gemm_bf16(const GemmArgs& a, int epi, int tile_cfg, hipStream_t st);
+// out[m][n] = bf16(GELU(sum_{s < S} part[s][m][n] + bias[n])), ranges added in
+// order s = 0, 1, ...; M * N elements, N a multiple of 4.
+hipError_t launch_splitk_gelu_bf16(const float* part, int S, int M, int N, const void* bias, void* out,
+                                   hipStream_t st);
 hipError_t launch_gemm_f32(const GemmArgs& a, int epi, hipStream_t st);
 hipError_t launch_attn_bf16(const AttnArgs& a, int head_dim, hipStream_t st);
 hipError_t launch_attn_f32(const AttnArgs& a, int head_dim, hipStream_t st);

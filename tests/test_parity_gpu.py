@@ -196,6 +196,16 @@ def test_block_c3_full_sampled_rows():
     block_case(synth.CONFIGS["c3"].with_(n_blocks=1), rows=rows)
 
 
+def test_block_joint_split_text_fc1():
+    """Joint block whose text-stream fc1 runs as k-range units in the last
+    round (image fc1 2048 x 8192 fills whole rounds of 256-row tiles; the 40
+    text rows are split into 4 k-ranges and reduced with bias and GELU after
+    the GEMM).  The text stream is compared in full."""
+    cfg = synth.CONFIGS["c3"].with_(batch=1, tokens=2048, text_tokens=40, hidden=1024, heads=8, head_dim=128,
+                                    mlp_hidden=8192, n_blocks=1)
+    block_case(cfg, rows=[0, 1, 1000, 2047])
+
+
 def test_block_c4_full_sampled_rows():
     rows = [0, 5, 8191, 12000, 17536, 17549]
     block_case(synth.CONFIGS["c4"].with_(n_blocks=1), rows=rows)
