@@ -78,6 +78,11 @@ SMALL = [
     # DiT-XL widths with ragged row counts that select the 256-row GEMM tiles:
     # 2000 rows -> QKV 256x128, fc1 256x256, out/fc2 64x144 (last M tile ragged)
     ("bf16_xl_t250_b8_tiles", synth.CONFIGS["c1"].with_(batch=8, tokens=250, n_blocks=1)),
+    # 4096 rows at hidden 576 and MLP 1728 (both multiples of 144, 9 and 27
+    # k-slices): the output projection and fc2 take the 64x144 tiles with a
+    # single k-group (odd slice count)
+    ("bf16_144_one_kgroup", synth.CONFIGS["c1"].with_(batch=4, tokens=1024, hidden=576, heads=8, head_dim=72,
+                                                      mlp_hidden=1728, n_blocks=1)),
     # 2340 rows -> QKV (incl. the v^T columns) and fc1 on 256x256 tiles
     ("bf16_xl_t260_b9_tiles", synth.CONFIGS["c1"].with_(batch=9, tokens=260, n_blocks=1)),
     # >= 256 (sample, head, 256-query) items select the software-pipelined
