@@ -216,11 +216,14 @@ def test_block_c4_full_sampled_rows():
     block_case(synth.CONFIGS["c4"].with_(n_blocks=1), rows=rows)
 
 
-def test_step_c1_full_end_to_end():
-    """Conditioning + the full 28-block step at the benchmarked workload."""
+@pytest.mark.parametrize("key", ["c1", "c2"])
+def test_step_full_end_to_end(key):
+    """Conditioning + the full 28-block step: DiT-XL/2 at 256 tokens x 8 (the
+    benchmarked workload) and at 1024 tokens x 4."""
     g = _gpu()
     import paper_2605_25550_amd as dm
-    cfg = synth.CONFIGS["c1"]
+    cfg = synth.CONFIGS[key]
+    print(f"[case] step {key} full", flush=True)
     sw = synth.step_weights(cfg)
     inp = synth.inputs(cfg)
     blocks = [synth.block_weights(cfg, l) for l in range(cfg.n_blocks)]
@@ -235,7 +238,7 @@ def test_step_c1_full_end_to_end():
     c = O.class_conditioning(inp["t"], inp["y"], *[sw[k].astype(np.float64) for k in
                                                     ("w_t1", "b_t1", "w_t2", "b_t2", "class_table")])
     rout, _ = step_ref(cfg, sw, blocks, inp, pos, c)
-    check("step/c1_full", out, rout, None, TOL["bf16"])
+    check(f"step/{key}_full", out, rout, None, TOL["bf16"])
 
 
 # ------------------------------------------------------------------ multi-step sampler loop
