@@ -67,6 +67,10 @@ def parse():
     ap.add_argument("--serve", type=int, default=0,
                     help="time N requests through dit_serve (copies in order vs overlapped on a second "
                          "stream) with --sample-steps (default 1) Euler steps each")
+    ap.add_argument("--sp-share", type=int, default=0, metavar="N",
+                    help="time one GPU's part of an N-way sequence-parallel step of --config: the token share "
+                         "(GEMMs, LayerNorm, embeddings on ceil(T/N) tokens, adaLN in full) and the head share "
+                         "(attention of H/N heads over all T tokens); the all-to-alls are not run")
     ap.add_argument("--sample-steps", type=int, default=0,
                     help="instead of single steps, time the multi-step Euler sampler loop of this many steps "
                          "(eager and replayed from a captured HIP graph)")
@@ -337,6 +341,65 @@ def serve_bench(wl, args, torch, dm):
                    "sampler": "euler", "steps": K}}), flush=True)
 
 
+def sp_share_bench(cfg, args, torch, dm):
+    """One GPU's part of an N-way Ulysses sequence-parallel step, measured on
+    one GPU.  Between the two all-to-alls of a block a GPU holds either
+    ceil(T/N) tokens with all heads (LayerNorm, the four GEMMs, patch embed,
+    final layer) or all T tokens of H/N heads (attention); the adaLN GEMV is
+    replicated.  Token share: a full step at ceil(T/N) tokens, minus its own
+    attention.  Head share: the attention launches of a step at H/N heads
+    (hidden D/N) over all T tokens.  Both are timed with HIP events on the
+    launch stream; the all-to-alls are not run (one GPU)."""
+    import math
+    N = args.sp_share
+    if cfg.joint or cfg.heads % N or cfg.hidden % (64 * N):
+        raise SystemExit("--sp-share needs a single-stream config with heads and hidden/64 divisible by N")
+    cfg_tok = cfg.with_(tokens=math.ceil(cfg.tokens / N))
+    cfg_head = cfg.with_(hidden=cfg.hidden // N, heads=cfg.heads // N, mlp_hidden=cfg.mlp_hidden // N)
+
+    def measure(c, classes):
+        wl = Workload(c, torch, dm)
+        for _ in range(args.warmup):
+            wl.step()
+        st = torch.cuda.current_stream()
+        ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        ev0.record(st)
+        for _ in range(args.steps):
+            wl.step()
+        ev1.record(st)
+        torch.cuda.synchronize()
+        step_ms = ev0.elapsed_time(ev1) / args.steps
+        per = {}
+        for k in classes:
+            dm.timing_enable(k, 8192)
+            for _ in range(args.steps):
+                wl.step()
+            torch.cuda.synchronize()
+            ms, n, _, _ = dm.timing_read()
+            dm.timing_disable()
+            per[k] = ms / args.steps
+        del wl
+        torch.cuda.empty_cache()
+        return step_ms, per
+
+    tok_ms, tok_cls = measure(cfg_tok, ["attention"])
+    _, head_cls = measure(cfg_head, ["attention"])
+    share_ms = tok_ms - tok_cls["attention"] + head_cls["attention"]
+    attn_flops = 4.0 * cfg.batch * (cfg.heads // N) * cfg.tokens ** 2 * cfg.head_dim * cfg.n_blocks
+    print(json.dumps({
+        "metric": f"one GPU's share of an {N}-way sequence-parallel DiT step (all-to-alls excluded), steps/s",
+        "value": round(1000.0 / share_ms, 3), "unit": "steps/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(share_ms, 4), "higher_is_better": True,
+        "token_share_step_ms": round(tok_ms, 4), "token_share_attention_ms": round(tok_cls["attention"], 4),
+        "head_share_attention_ms": round(head_cls["attention"], 4),
+        "head_share_attention_tflops": round(attn_flops / (head_cls["attention"] * 1e-3) / 1e12, 1),
+        "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": f"{cfg.name}_sp{N}_share", "blocks": cfg.n_blocks, "tokens": cfg.tokens,
+                   "token_share": cfg_tok.tokens, "heads": cfg.heads, "head_share": cfg_head.heads,
+                   "hidden": cfg.hidden, "head_dim": cfg.head_dim, "mlp_hidden": cfg.mlp_hidden}}), flush=True)
+
+
 def main():
     args = parse()
     if args.summarize_pmc:
@@ -358,6 +421,9 @@ def main():
         raise SystemExit("bench.py times the bf16 workloads (c1..c4)")
     torch.cuda.set_device(0)
     dm.lib()
+    if args.sp_share:
+        sp_share_bench(cfg, args, torch, dm)
+        return
     wl = Workload(cfg, torch, dm)
     st = torch.cuda.current_stream()
     if args.serve:

@@ -625,11 +625,14 @@ __global__ __launch_bounds__(NW * 64, WPC) void attn_bf16_pipe_kernel(AttnArgs a
 }
 
 hipError_t launch_attn_bf16(const AttnArgs& a, int head_dim, hipStream_t st) {
-  // Enough work items for every CU: the pipelined kernel, 8 waves x 32
-  // queries per workgroup.  Otherwise (few, short sequences) the first
+  // Enough work items for every CU, or at least half of them with long
+  // sequences (32 key tiles or more, where the steady state dominates, e.g.
+  // 3 heads over 17550 tokens: 207 items): the pipelined kernel, 8 waves x
+  // 32 queries per workgroup.  Otherwise (few, short sequences) the first
   // kernel with 4 waves x 32 queries, which spreads the work over twice as
   // many workgroups.
-  const bool wide = (long)((a.Tj + 255) / 256) * a.H * a.B >= 256;
+  const long items = (long)((a.Tj + 255) / 256) * a.H * a.B;
+  const bool wide = items >= 256 || (items >= 128 && a.Tj >= 2048);
   const int nw = wide ? 8 : 4;
   dim3 grid((a.Tj + nw * 32 - 1) / (nw * 32), a.H, a.B), block(nw * 64);
 #define ATTN_LAUNCH(DHV)                                                                   \

@@ -216,6 +216,19 @@ def test_block_c4_full_sampled_rows():
     block_case(synth.CONFIGS["c4"].with_(n_blocks=1), rows=rows)
 
 
+def test_block_c4_sp8_token_share():
+    """One GPU's token share of an 8-way sequence-parallel video DiT step:
+    ceil(17550 / 8) = 2194 tokens with all 24 heads (a ragged last row tile)."""
+    block_case(synth.CONFIGS["c4"].with_(tokens=2194, n_blocks=1), rows=[0, 1, 1000, 2193])
+
+
+def test_block_c4_sp8_head_share():
+    """One GPU's head share of an 8-way sequence-parallel video DiT step:
+    attention of 3 heads x 128 over all 17550 tokens (hidden 384)."""
+    block_case(synth.CONFIGS["c4"].with_(hidden=384, heads=3, mlp_hidden=1536, n_blocks=1),
+               rows=[0, 5, 9000, 17549])
+
+
 @pytest.mark.parametrize("key", ["c1", "c2"])
 def test_step_full_end_to_end(key):
     """Conditioning + the full 28-block step: DiT-XL/2 at 256 tokens x 8 (the
