@@ -211,6 +211,16 @@ def test_block_joint_split_text_fc1():
     block_case(cfg, rows=[0, 1, 1000, 2047])
 
 
+def test_block_joint_split_text_fc1_deterministic():
+    """The split ranges are added in a fixed order: two runs agree bitwise."""
+    g = _gpu()
+    cfg = synth.CONFIGS["c3"].with_(batch=1, tokens=2048, text_tokens=40, hidden=1024, heads=8, head_dim=128,
+                                    mlp_hidden=8192, n_blocks=1)
+    inp = synth.inputs(cfg)
+    (y1, t1), (y2, t2) = g.run_block(cfg, synth.block_weights(cfg, 0), inp["x"], inp["cond"], inp["x_txt"], repeat=2)
+    assert np.array_equal(y1, y2) and np.array_equal(t1, t2)
+
+
 def test_block_c4_full_sampled_rows():
     rows = [0, 5, 8191, 12000, 17536, 17549]
     block_case(synth.CONFIGS["c4"].with_(n_blocks=1), rows=rows)
