@@ -56,6 +56,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--config", default="c1", help="workload key (c1 is the reported one)")
+    ap.add_argument("--batch", type=int, default=0, help="override the workload's batch size (0: as configured)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-blocks", type=int, default=28, help="oracle blocks in the CPU sample")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
@@ -417,6 +418,8 @@ def main():
     import synth
 
     cfg = synth.CONFIGS[args.config]
+    if args.batch and args.batch != cfg.batch:  # its own workload name; no traffic record applies
+        cfg = cfg.with_(batch=args.batch, key=f"{cfg.key}_batch{args.batch}", name=f"{cfg.name}_batch{args.batch}")
     if cfg.dtype != "bf16":
         raise SystemExit("bench.py times the bf16 workloads (c1..c4)")
     torch.cuda.set_device(0)

@@ -75,8 +75,35 @@ struct Layout {
   size_t t, vel, cond, xt;  // sampler loop: timesteps [B], velocity [B,T,P], c [B,D], text states [B,Tt,D]
   size_t slot_z[2], slot_y[2], slot_c[2];  // serving: two request slots
   size_t qk;  // q/k row length (elements)
+  size_t part, part_cap;  // fp32 partials of split GEMMs: the dead q/k/v region, or a region of its own
   int ns, Tj, Tj_pad;
 };
+
+int choose_tile(const GemmProb* p, int np, int epi, size_t part_cap, int* split);
+
+// Bytes of fp32 partials the split GEMMs of this shape need (the largest of
+// the output projection, fc1 and fc2; 0 if none is split).
+static size_t split_part_bytes(const dit_shape* s) {
+  if (s->dtype != DIT_BF16) return 0;
+  const int ns = s->text_tokens > 0 ? 2 : 1;
+  const int D = s->hidden, F = s->mlp_hidden;
+  const int gemms[3][3] = {{EPI_RESID, D, D}, {EPI_GELU, F, D}, {EPI_RESID2, D, F}};  // epilogue, N, K
+  size_t need = 0;
+  for (const auto& g : gemms) {
+    GemmProb p[2] = {};
+    for (int i = 0; i < ns; ++i) {
+      p[i].M = s->batch * (i ? s->text_tokens : s->tokens);
+      p[i].N = g[1];
+      p[i].K = g[2];
+      p[i].hidden = D;
+    }
+    int S = 0;
+    choose_tile(p, ns, g[0], SIZE_MAX, &S);
+    const size_t b = (size_t)S * p[ns - 1].M * p[ns - 1].N * 4;
+    if (b > need) need = b;
+  }
+  return need;
+}
 
 Layout layout(const dit_shape* s, int kind) {
   Layout L{};
@@ -110,6 +137,11 @@ Layout layout(const dit_shape* s, int kind) {
   L.v = take(E == 2 ? B * H * dh * (size_t)L.Tj_pad * 2 : B * H * L.Tj * dh * 4);
   L.o = take(rows * D * E);
   L.g = take(rows * F * E);
+  {
+    const size_t need = split_part_bytes(s), span = L.o - L.q;
+    L.part = need <= span ? L.q : take(need);
+    L.part_cap = need <= span ? span : need;
+  }
   L.x = step ? take(B * T * D * 4) : 0;
   if (kind == DIT_WS_SAMPLE || kind == DIT_WS_SERVE) {
     L.t = take(B * 4);
@@ -176,7 +208,7 @@ struct Gemm {
   int epi = EPI_STORE;
   int kclass = DIT_K_OTHER;
   double flops = 0, bytes = 0;
-  float* part = nullptr;  // fp32 scratch for a split second problem (EPI_GELU), part_cap bytes
+  float* part = nullptr;  // fp32 scratch for a split problem, part_cap bytes
   size_t part_cap = 0;
 };
 
@@ -224,6 +256,26 @@ static int tail_split(const GemmProb* p, int np, int epi, int bm, int bn, size_t
 // of a round.
 static double tail_rounds(long t0, int S) { return (double)(t0 / 256) + 1.0 / S + 0.15; }
 
+// Fill split: a single problem whose tiles cannot fill the GPU (at most 128
+// tiles, e.g. the DiT-XL/2 fc2 at one sample of 256 tokens: 36 tiles of
+// 64 x 128, each 72 k-slices long) is split into S equal k-ranges of at
+// least 4 slices, with at most 256 units in all, when the estimated gain
+//   (1 - 1/S) * 0.45 us per slice - partial traffic at 5 TB/s - 3 us
+// of reduction launch is positive.  Returns S (0: no split).
+static int fill_split(const GemmProb& p, int epi, int bm, int bn, size_t part_cap) {
+  if ((epi != EPI_GELU && epi != EPI_RESID && epi != EPI_RESID2) || part_cap == 0) return 0;
+  const long t = (long)((p.M + bm - 1) / bm) * ((p.N + bn - 1) / bn);
+  const int ks = p.K / 64;
+  if (t == 0 || t > 128) return 0;
+  for (int S = 8; S >= 2; --S) {
+    if (t * S > 256 || ks % S != 0 || ks / S < 4 || (size_t)S * p.M * p.N * 4 > part_cap) continue;
+    const double mn = (double)p.M * p.N;
+    const double gain_us = (1.0 - 1.0 / S) * ks * 0.45 - (S * 4.0 + 8.0) * mn / 5e6 - 3.0;
+    if (gain_us > 0) return S;
+  }
+  return 0;
+}
+
 int choose_tile(const GemmProb* p, int np, int epi, size_t part_cap, int* split) {
   *split = 0;
   long t128 = 0, t144 = 0, t256 = 0, t2x1 = 0, t192 = 0;
@@ -260,9 +312,15 @@ int choose_tile(const GemmProb* p, int np, int epi, size_t part_cap, int* split)
       return best;
     }
   }
-  if ((t128 >= 256 && t128 < 512) || t128 >= 768) return TILE_128x128;
-  if (t128 >= 512) return TILE_64x128_S2;
-  return TILE_64x128;
+  const int cfg = ((t128 >= 256 && t128 < 512) || t128 >= 768) ? TILE_128x128
+                  : t128 >= 512                                   ? TILE_64x128_S2
+                                                                  : TILE_64x128;
+  if (np == 1) {
+    int bm = 0, bn = 0;
+    gemm_tile_dims(cfg, &bm, &bn);
+    *split = fill_split(p[0], epi, bm, bn, part_cap);
+  }
+  return cfg;
 }
 
 hipError_t run_gemm(Gemm& G, int dtype, hipStream_t st) {
@@ -282,21 +340,29 @@ hipError_t run_gemm(Gemm& G, int dtype, hipStream_t st) {
     p.part = nullptr;
     tiles += p.tiles_m * p.tiles_n * (i == 1 && split ? split : 1);
   }
+  // The split problem is the second of two (tail schedule) or the only one
+  // (fill split, every unit in one round, the usual tile order).
+  const int sp = a.nprob - 1;
+  if (split && sp == 0) tiles *= split;
   a.total_tiles = tiles;
-  a.tail = split ? 1 : 0;
+  a.tail = split && sp == 1 ? 1 : 0;
   if (split) {
-    a.p[1].ksplit = split;
-    a.p[1].part = G.part;
+    a.p[sp].ksplit = split;
+    a.p[sp].part = G.part;
   }
   if (tiles == 0) return hipSuccess;
   hipError_t e = timed(G.kclass, G.flops, G.bytes, st, [&]() {
     return dtype == DIT_BF16 ? launch_gemm_bf16(a, G.epi, tcfg, st) : launch_gemm_f32(a, G.epi, st);
   });
   if (e != hipSuccess || !split) return e;
-  const GemmProb& p1 = a.p[1];
-  const double mn = (double)p1.M * p1.N;
-  return timed(DIT_K_OTHER, 0, mn * (split * 4.0 + 2.0) + p1.N * 2.0, st, [&]() {
-    return launch_splitk_gelu_bf16(p1.part, split, p1.M, p1.N, p1.bias, p1.out, st);
+  const GemmProb& q = a.p[sp];
+  const double mn = (double)q.M * q.N;
+  if (G.epi == EPI_GELU)
+    return timed(DIT_K_OTHER, 0, mn * (split * 4.0 + 2.0) + q.N * 2.0, st, [&]() {
+      return launch_splitk_gelu_bf16(q.part, split, q.M, q.N, q.bias, q.out, st);
+    });
+  return timed(DIT_K_OTHER, 0, mn * (split * 4.0 + 8.0) + q.N * 2.0, st, [&]() {
+    return launch_splitk_resid(q.part, split, q.M, q.N, q.bias, q.gate, q.gate_stride, q.rows_per_batch, q.resid, st);
   });
 }
 
@@ -422,6 +488,10 @@ dit_status run_block(const dit_shape* s, const Layout& L, char* ws, StreamIO* io
       p.gate = io[i].mod + 2 * D;
       p.gate_stride = 6 * D;
     }
+    // fp32 partials of a split GEMM: q, k and v are dead after attention
+    // (where their region is too small the workspace has one of its own)
+    G.part = (float*)(ws + L.part);
+    G.part_cap = L.part_cap;
     G.flops = 2.0 * tokens * D * D;
     G.bytes = (tokens * D + ns * (double)D * D) * E + tokens * D * 8.0;
     HIP_TRY(run_gemm(G, dt, st));
@@ -439,10 +509,8 @@ dit_status run_block(const dit_shape* s, const Layout& L, char* ws, StreamIO* io
       prob_common(p, i, act(h, i, D), io[i].w->w_fc1, io[i].w->b_fc1, F, D);
       p.out = act(gbuf, i, F);
     }
-    // q, k and v are dead after attention: their region holds the fp32
-    // partials of a split text-stream problem.
-    G.part = (float*)(ws + L.q);
-    G.part_cap = L.o - L.q;
+    G.part = (float*)(ws + L.part);
+    G.part_cap = L.part_cap;
     G.flops = 2.0 * tokens * F * D;
     G.bytes = (tokens * D + ns * (double)F * D + tokens * F) * E;
     HIP_TRY(run_gemm(G, dt, st));
@@ -460,6 +528,8 @@ dit_status run_block(const dit_shape* s, const Layout& L, char* ws, StreamIO* io
       p.gate = io[i].mod + 5 * D;
       p.gate_stride = 6 * D;
     }
+    G.part = (float*)(ws + L.part);
+    G.part_cap = L.part_cap;
     G.flops = 2.0 * tokens * D * F;
     G.bytes = (tokens * F + ns * (double)D * F) * E + tokens * D * 8.0;
     HIP_TRY(run_gemm(G, dt, st));

@@ -116,7 +116,7 @@ struct Epilogue {
 
   // Residual rows of the slab at global row mb (EPI_RESID only).
   __device__ __forceinline__ void load_resid(f32x4 (&x)[NX], const GemmProb& P, int mb, int nw0, int lane) const {
-    if (!RES) return;
+    if (!RES || P.ksplit > 1) return;  // a split unit stores a raw partial
 #pragma unroll
     for (int it = 0; it < PL; ++it) {
       const int c = lane + 64 * it;
@@ -177,6 +177,10 @@ struct Epilogue {
       const int m = mb + row, n = nw0 + c4;
       if (m >= M || n >= N) continue;  // N is a multiple of 4
       const f32x4 y = cy[it];
+      if ((RES || EPI == EPI_GELU) && P.ksplit > 1) {  // one k-range: raw fp32 partial (P.part at its range)
+        *(f32x4*)(P.part + (long)m * N + n) = y;
+        continue;
+      }
       const f32x4 bq = bias4[it % NCG];
       const float y0 = y[0] + bq[0], y1 = y[1] + bq[1], y2 = y[2] + bq[2], y3 = y[3] + bq[3];
       if (RES) {
@@ -189,8 +193,6 @@ struct Epilogue {
         xv[2] += g[2] * y2;
         xv[3] += g[3] * y3;
         *(f32x4*)(P.resid + (long)m * N + n) = xv;
-      } else if (EPI == EPI_GELU && P.ksplit > 1) {  // one k-range: raw fp32 partial (P.part at its range)
-        *(f32x4*)(P.part + (long)m * N + n) = y;
       } else if (EPI == EPI_GELU) {
         *(u32x2*)((bf16_t*)P.out + (long)m * N + n) =
             u32x2{pack_bf16x2(gelu_tanh(y0), gelu_tanh(y1)), pack_bf16x2(gelu_tanh(y2), gelu_tanh(y3))};
@@ -431,7 +433,7 @@ __global__ __launch_bounds__(WGM * WGN * 64) void gemm_bf16_kernel(GemmArgs args
   // Split K: unit u of the problem is k-range u / (tiles_m tiles_n) of tile
   // u % (tiles_m tiles_n).
   int local = tile - P.tile_begin, kb = 0, nks = P.K / C::BK;
-  if (EPI == EPI_GELU && P.ksplit > 1) {
+  if ((EPI == EPI_GELU || EPI == EPI_RESID || EPI == EPI_RESID2) && P.ksplit > 1) {
     const int per = P.tiles_m * P.tiles_n, s = local / per;
     local -= s * per;
     nks /= P.ksplit;
@@ -698,6 +700,44 @@ hipError_t launch_splitk_gelu_bf16(const float* part, int S, int M, int N, const
   const long groups = MN / 4;
   hipLaunchKernelGGL(splitk_gelu_kernel, dim3((unsigned)((groups + 255) / 256)), dim3(256), 0, st, part, S, MN, N,
                      (const bf16_t*)bias, (bf16_t*)out);
+  return hipGetLastError();
+}
+
+// Split-K reduction into the fp32 residual: four consecutive outputs per
+// lane; the ranges are added in order, then the bias, then the gated update
+// as in the GEMM's residual epilogue.
+__global__ __launch_bounds__(256) void splitk_resid_kernel(const float* __restrict__ part, int S, long MN, int N,
+                                                           const bf16_t* __restrict__ bias,
+                                                           const float* __restrict__ gate, int gate_stride,
+                                                           int rows_per_batch, float* __restrict__ resid) {
+  const long e = (blockIdx.x * 256L + threadIdx.x) * 4;
+  if (e >= MN) return;
+  f32x4 y = *(const f32x4*)(part + e);
+  for (int s = 1; s < S; ++s) {
+    const f32x4 p = *(const f32x4*)(part + s * MN + e);
+    y[0] += p[0];
+    y[1] += p[1];
+    y[2] += p[2];
+    y[3] += p[3];
+  }
+  const long m = e / N;
+  const int n = (int)(e - m * N), b = (int)(m / rows_per_batch);
+  const u32x2 w = *(const u32x2*)(bias + n);
+  const f32x4 g = *(const f32x4*)(gate + (long)b * gate_stride + n);
+  f32x4 x = *(const f32x4*)(resid + e);
+  x[0] += g[0] * (y[0] + __uint_as_float(w[0] << 16));
+  x[1] += g[1] * (y[1] + __uint_as_float(w[0] & 0xFFFF0000u));
+  x[2] += g[2] * (y[2] + __uint_as_float(w[1] << 16));
+  x[3] += g[3] * (y[3] + __uint_as_float(w[1] & 0xFFFF0000u));
+  *(f32x4*)(resid + e) = x;
+}
+
+hipError_t launch_splitk_resid(const float* part, int S, int M, int N, const void* bias, const float* gate,
+                               int gate_stride, int rows_per_batch, float* resid, hipStream_t st) {
+  const long MN = (long)M * N;
+  if (MN == 0) return hipSuccess;
+  hipLaunchKernelGGL(splitk_resid_kernel, dim3((unsigned)((MN / 4 + 255) / 256)), dim3(256), 0, st, part, S, MN, N,
+                     (const bf16_t*)bias, gate, gate_stride, rows_per_batch, resid);
   return hipGetLastError();
 }
 

@@ -38,10 +38,11 @@ struct GemmProb {
   int qk_stride;       // q/k row length: head_dim, or (bf16) head_dim rounded up to 16, padded with
                        // zeros except k's column head_dim, which holds 1
   float k_scale;       // bf16: k is stored multiplied by this (log2(e)/sqrt(dh), the softmax's exp2 scale)
-  // Split K (bf16, EPI_GELU, second problem only): ksplit > 1 divides the
+  // Split K (bf16; EPI_GELU, EPI_RESID, EPI_RESID2): ksplit > 1 divides the
   // k-slices into ksplit equal ranges; the unit of tile t and range s stores
   // its fp32 product without bias to part[s][M][N], and
-  // launch_splitk_gelu_bf16 then adds the ranges, the bias and the GELU.
+  // launch_splitk_gelu_bf16 / launch_splitk_resid then add the ranges and
+  // apply the epilogue.
   float* part;
   int ksplit;
 };
@@ -113,6 +114,10 @@ hipError_t launch_gemm_bf16(const GemmArgs& a, int epi, int tile_cfg, hipStream_
 // order s = 0, 1, ...; M * N elements, N a multiple of 4.
 hipError_t launch_splitk_gelu_bf16(const float* part, int S, int M, int N, const void* bias, void* out,
                                    hipStream_t st);
+// resid[m][n] += gate[b * gate_stride + n] * (sum_{s < S} part[s][m][n] + bias[n]),
+// b = m / rows_per_batch, ranges added in order s = 0, 1, ...; bf16 bias.
+hipError_t launch_splitk_resid(const float* part, int S, int M, int N, const void* bias, const float* gate,
+                               int gate_stride, int rows_per_batch, float* resid, hipStream_t st);
 hipError_t launch_gemm_f32(const GemmArgs& a, int epi, hipStream_t st);
 hipError_t launch_attn_bf16(const AttnArgs& a, int head_dim, hipStream_t st);
 hipError_t launch_attn_f32(const AttnArgs& a, int head_dim, hipStream_t st);

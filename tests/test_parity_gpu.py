@@ -83,6 +83,12 @@ SMALL = [
     # single k-group (odd slice count)
     ("bf16_144_one_kgroup", synth.CONFIGS["c1"].with_(batch=4, tokens=1024, hidden=576, heads=8, head_dim=72,
                                                       mlp_hidden=1728, n_blocks=1)),
+    # DiT-XL widths at one or two samples: the output projection and fc2 run
+    # too few 64x128 tiles to fill the GPU and are split into k-ranges
+    # (fc2 at 256 rows: 36 tiles x 6 ranges; 250 rows: a ragged row tile)
+    ("bf16_xl_b1_split", synth.CONFIGS["c1"].with_(batch=1, n_blocks=1)),
+    ("bf16_xl_b1_t250_split", synth.CONFIGS["c1"].with_(batch=1, tokens=250, n_blocks=1)),
+    ("bf16_xl_b2_split", synth.CONFIGS["c1"].with_(batch=2, n_blocks=1)),
     # 2340 rows -> QKV (incl. the v^T columns) and fc1 on 256x256 tiles
     ("bf16_xl_t260_b9_tiles", synth.CONFIGS["c1"].with_(batch=9, tokens=260, n_blocks=1)),
     # >= 256 (sample, head, 256-query) items select the software-pipelined
