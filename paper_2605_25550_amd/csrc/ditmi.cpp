@@ -256,19 +256,24 @@ static int tail_split(const GemmProb* p, int np, int epi, int bm, int bn, size_t
 // of a round.
 static double tail_rounds(long t0, int S) { return (double)(t0 / 256) + 1.0 / S + 0.15; }
 
-// Fill split: a single problem whose tiles cannot fill the GPU (at most 128
-// tiles, e.g. the DiT-XL/2 fc2 at one sample of 256 tokens: 36 tiles of
-// 64 x 128, each 72 k-slices long) is split into S equal k-ranges of at
-// least 4 slices, with at most 256 units in all, when the estimated gain
+// Fill split: a single problem whose tiles cannot fill the GPU is split
+// into S equal k-ranges of at least 4 slices, e.g. the DiT-XL/2 fc2 at one
+// sample of 256 tokens: 36 tiles of 64 x 128, each 72 k-slices long, as 216
+// units of 12 slices.  Up to 128 tiles the units are at most one per CU
+// (256; measured faster than more, smaller units sharing CUs); up to half
+// of `slots` (the workgroups resident at once: 256 CUs x workgroups per CU)
+// they may fill the slots.  S is the largest such split for which the
+// estimated gain
 //   (1 - 1/S) * 0.45 us per slice - partial traffic at 5 TB/s - 3 us
 // of reduction launch is positive.  Returns S (0: no split).
-static int fill_split(const GemmProb& p, int epi, int bm, int bn, size_t part_cap) {
+static int fill_split(const GemmProb& p, int epi, int bm, int bn, long slots, size_t part_cap) {
   if ((epi != EPI_GELU && epi != EPI_RESID && epi != EPI_RESID2) || part_cap == 0) return 0;
   const long t = (long)((p.M + bm - 1) / bm) * ((p.N + bn - 1) / bn);
   const int ks = p.K / 64;
-  if (t == 0 || t > 128) return 0;
+  if (t == 0 || 2 * t > slots) return 0;
+  const long units = t <= 128 ? 256 : slots;
   for (int S = 8; S >= 2; --S) {
-    if (t * S > 256 || ks % S != 0 || ks / S < 4 || (size_t)S * p.M * p.N * 4 > part_cap) continue;
+    if (t * S > units || ks % S != 0 || ks / S < 4 || (size_t)S * p.M * p.N * 4 > part_cap) continue;
     const double mn = (double)p.M * p.N;
     const double gain_us = (1.0 - 1.0 / S) * ks * 0.45 - (S * 4.0 + 8.0) * mn / 5e6 - 3.0;
     if (gain_us > 0) return S;
@@ -318,7 +323,9 @@ int choose_tile(const GemmProb* p, int np, int epi, size_t part_cap, int* split)
   if (np == 1) {
     int bm = 0, bn = 0;
     gemm_tile_dims(cfg, &bm, &bn);
-    *split = fill_split(p[0], epi, bm, bn, part_cap);
+    // resident workgroups per CU (LDS): 128x128 and 64x128 with 3 slots two, 64x128 with 2 slots three
+    const long per_cu = cfg == TILE_64x128_S2 ? 3 : 2;
+    *split = fill_split(p[0], epi, bm, bn, 256 * per_cu, part_cap);
   }
   return cfg;
 }

@@ -89,6 +89,7 @@ SMALL = [
     ("bf16_xl_b1_split", synth.CONFIGS["c1"].with_(batch=1, n_blocks=1)),
     ("bf16_xl_b1_t250_split", synth.CONFIGS["c1"].with_(batch=1, tokens=250, n_blocks=1)),
     ("bf16_xl_b2_split", synth.CONFIGS["c1"].with_(batch=2, n_blocks=1)),
+    ("bf16_xl_b4_split", synth.CONFIGS["c1"].with_(batch=4, n_blocks=1)),
     # 2340 rows -> QKV (incl. the v^T columns) and fc1 on 256x256 tiles
     ("bf16_xl_t260_b9_tiles", synth.CONFIGS["c1"].with_(batch=9, tokens=260, n_blocks=1)),
     # >= 256 (sample, head, 256-query) items select the software-pipelined
