@@ -35,13 +35,13 @@
  *     they propagate.  No call aborts or throws.
  *   - dit_last_error() returns the text of the calling thread's last failure.
  *   - Calls are thread-safe; concurrent calls must not share a workspace.
- *   - dit_step_forward may enqueue advisory work on one internal stream per
- *     (calling thread, device), created at first use with default priority:
- *     reads of the next block's weights into the Infinity Cache.  It is
- *     forked from and joined back into `stream` with events inside the call,
- *     so all later work on `stream` (including freeing the weights) is
- *     ordered after it, and the call can be captured into a HIP graph.
- *     No allocation or memset is enqueued by any call.
+ *   - Every kernel of a call runs on `stream`; the library creates no
+ *     streams.  No allocation or memset is enqueued by any call, so the
+ *     calls can be captured into a HIP graph.
+ *   - Size limits (DIT_ERR_UNSUPPORTED beyond them): rows = B * (T + Tt)
+ *     below 2^24 with rows * max(3D, F) below 2^31, and every weight matrix
+ *     (in particular F * D) below 2^31 elements, so that all byte offsets
+ *     inside one operand fit the kernels' 32-bit address arithmetic.
  */
 #ifndef DITMI_H
 #define DITMI_H

@@ -61,6 +61,13 @@ dit_status check_shape(const dit_shape* s, bool step) {
   const long widest = s->mlp_hidden > 3 * s->hidden ? s->mlp_hidden : 3L * s->hidden;
   if (rows * widest >= (1L << 31) || rows >= (1L << 24))
     return fail(DIT_ERR_UNSUPPORTED, "batch*tokens (%ld rows) too large", rows);
+  // The GEMM's DMA lane offsets (row * K * 2 bytes) and the adaLN/GEMV row
+  // offsets are 32-bit: every weight matrix stays below 2^31 elements.  The
+  // largest are fc1 / fc2 with F * D elements (w_ada 6 D^2 and w_qkv 3 D^2
+  // are bounded by hidden <= 4096).
+  if ((long)s->mlp_hidden * s->hidden >= (1L << 31))
+    return fail(DIT_ERR_UNSUPPORTED, "mlp_hidden * hidden (%d * %d) >= 2^31 elements: weight matrix too large",
+                s->mlp_hidden, s->hidden);
   if (step) {
     if (s->n_blocks < 1) return fail(DIT_ERR_INVALID_ARG, "n_blocks (%d) must be >= 1", s->n_blocks);
     if (s->patch_in < 1 || s->patch_in > 256 || s->patch_out < 4 || s->patch_out > 256 || s->patch_out % 4 != 0)

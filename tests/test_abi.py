@@ -75,6 +75,21 @@ def test_workspace_rejects_bad_shapes(dm, field, value, status):
     assert dm.last_error()
 
 
+def test_weight_matrix_size_limit(dm):
+    """A weight matrix of 2^31 or more elements (F * D) is rejected before any
+    launch: the kernels address one operand with 32-bit byte offsets.  Hidden
+    4096 with MLP width 524288 is a 4 GiB fc1 weight, which the HBM could
+    hold; one width step below the limit is accepted."""
+    s = shape(dm, "c1", batch=1, tokens=16, hidden=4096, heads=32, head_dim=128, mlp_hidden=524288)
+    lib = dm.lib()
+    assert lib.dit_workspace_bytes(ctypes.byref(s), 0) == 0
+    assert "mlp_hidden" in dm.last_error()
+    bw = fake_block(dm)
+    assert block_call(dm, s, bw) == -2
+    s.mlp_hidden = 524288 - 64
+    assert lib.dit_workspace_bytes(ctypes.byref(s), 0) > 0
+
+
 FAKE = 0x100000  # 1 MiB-aligned fake device address; never dereferenced
 
 

@@ -260,6 +260,109 @@ def test_joint_text_stream_uses_its_own_weights():
     np.testing.assert_allclose(yt_r, yt_a, rtol=0, atol=1e-13)
 
 
+def torch_joint_block(xi, xt, c, wi, wt, heads, eps=1e-6):
+    """Independent two-stream composition from torch float64 library routines:
+    each stream's adaLN, LayerNorm, modulation, QKV, output projection and MLP
+    use that stream's own weights; one scaled_dot_product_attention runs over
+    the concatenated [image; text] q, k and v."""
+    t = lambda a: torch.from_numpy(np.asarray(a, dtype=np.float64))
+    c = t(c)
+    xs = [t(xi), t(xt)]
+    ws = [wi, wt]
+    B, D = c.shape
+    mods = [F.linear(F.silu(c), t(w["w_ada"]), t(w["b_ada"])).chunk(6, dim=-1) for w in ws]
+    qkvs = []
+    for x, w, m in zip(xs, ws, mods):
+        h = F.layer_norm(x, (D,), eps=eps) * (1 + m[1][:, None]) + m[0][:, None]
+        T = x.shape[1]
+        qkvs.append(F.linear(h, t(w["w_qkv"]), t(w["b_qkv"])).reshape(B, T, 3, heads, D // heads).permute(2, 0, 3, 1, 4))
+    qkv = torch.cat(qkvs, dim=3)
+    o = F.scaled_dot_product_attention(qkv[0], qkv[1], qkv[2]).transpose(1, 2).reshape(B, -1, D)
+    Ti = xs[0].shape[1]
+    outs = []
+    for x, w, m, oo in zip(xs, ws, mods, (o[:, :Ti], o[:, Ti:])):
+        x = x + m[2][:, None] * F.linear(oo, t(w["w_o"]), t(w["b_o"]))
+        h2 = F.layer_norm(x, (D,), eps=eps) * (1 + m[4][:, None]) + m[3][:, None]
+        u = F.gelu(F.linear(h2, t(w["w_fc1"]), t(w["b_fc1"])), approximate="tanh")
+        outs.append((x + m[5][:, None] * F.linear(u, t(w["w_fc2"]), t(w["b_fc2"]))).numpy())
+    return outs[0], outs[1]
+
+
+def _distinct_stream_weights(cfg):
+    """Image and text weights that differ in every tensor, with the text set's
+    values scaled up so that routing an image tensor into the text stream (or
+    the reverse) moves the result far beyond rounding."""
+    wi = weights(cfg, stream=0)
+    wt = {k: v * 3.0 for k, v in weights(cfg, stream=1).items()}
+    return wi, wt
+
+
+def test_joint_matches_torch_two_stream_composition():
+    """Pins the per-stream routing of every weight of the joint block."""
+    cfg = tiny_cfg(text_tokens=6)
+    wi, wt = _distinct_stream_weights(cfg)
+    xi = rand((cfg.batch, cfg.tokens, cfg.hidden), 35)
+    xt = rand((cfg.batch, 6, cfg.hidden), 36)
+    c = rand((cfg.batch, cfg.hidden), 37)
+    yi, yt = O.joint_block(xi, xt, c, wi, wt, cfg.heads)
+    ri, rt = torch_joint_block(xi, xt, c, wi, wt, cfg.heads)
+    np.testing.assert_allclose(yi, ri, rtol=0, atol=1e-10)
+    np.testing.assert_allclose(yt, rt, rtol=0, atol=1e-10)
+
+
+@pytest.mark.parametrize("name", ["w_ada", "b_ada", "w_qkv", "b_qkv", "w_o", "b_o", "w_fc1", "b_fc1", "w_fc2", "b_fc2"])
+def test_joint_each_text_weight_routes_to_text_stream(name):
+    """Replacing one text-stream tensor changes the result exactly as the
+    torch composition predicts (and for the tensors after attention, only
+    the text rows)."""
+    cfg = tiny_cfg(text_tokens=5)
+    wi, wt = _distinct_stream_weights(cfg)
+    xi = rand((cfg.batch, cfg.tokens, cfg.hidden), 38)
+    xt = rand((cfg.batch, 5, cfg.hidden), 39)
+    c = rand((cfg.batch, cfg.hidden), 40)
+    wt2 = dict(wt)
+    wt2[name] = wt[name] + rand(wt[name].shape, 41) * 0.05
+    yi, yt = O.joint_block(xi, xt, c, wi, wt2, cfg.heads)
+    ri, rt = torch_joint_block(xi, xt, c, wi, wt2, cfg.heads)
+    np.testing.assert_allclose(yi, ri, rtol=0, atol=1e-10)
+    np.testing.assert_allclose(yt, rt, rtol=0, atol=1e-10)
+    yi0, yt0 = O.joint_block(xi, xt, c, wi, wt, cfg.heads)
+    assert not np.allclose(yt, yt0)
+    if name in ("w_o", "b_o", "w_fc1", "b_fc1", "w_fc2", "b_fc2"):
+        assert np.array_equal(yi, yi0)
+
+
+def _zero_gate_rows(w, D):
+    w = dict(w)
+    for k in ("w_ada", "b_ada"):
+        a = w[k].copy()
+        a[2 * D:3 * D] = 0.0
+        a[5 * D:6 * D] = 0.0
+        w[k] = a
+    return w
+
+
+def test_joint_zero_gates_per_stream():
+    """Zero gates in one stream make that stream the identity (bitwise) and
+    leave the other stream's branches active."""
+    cfg = tiny_cfg(text_tokens=5)
+    wi, wt = _distinct_stream_weights(cfg)
+    D = cfg.hidden
+    xi = rand((cfg.batch, cfg.tokens, D), 42)
+    xt = rand((cfg.batch, 5, D), 43)
+    c = rand((cfg.batch, D), 44)
+    yi, yt = O.joint_block(xi, xt, c, wi, _zero_gate_rows(wt, D), cfg.heads)
+    assert np.array_equal(yt, xt)
+    assert not np.allclose(yi, xi)
+    ri, _ = torch_joint_block(xi, xt, c, wi, _zero_gate_rows(wt, D), cfg.heads)
+    np.testing.assert_allclose(yi, ri, rtol=0, atol=1e-10)
+    yi, yt = O.joint_block(xi, xt, c, _zero_gate_rows(wi, D), wt, cfg.heads)
+    assert np.array_equal(yi, xi)
+    assert not np.allclose(yt, xt)
+    _, rt = torch_joint_block(xi, xt, c, _zero_gate_rows(wi, D), wt, cfg.heads)
+    np.testing.assert_allclose(yt, rt, rtol=0, atol=1e-10)
+
+
 # ------------------------------------------------------------ elementwise pieces
 def test_gelu_tanh_identities_and_library():
     u = np.linspace(-7, 7, 1001)

@@ -324,7 +324,7 @@ def test_sample_euler_graph_replay():
     g, dm, sw, blocks, inp, ds, ws, kw = _sample_setup(cfg)
     z0 = g.dev(inp["patches"])
     z_eager = z0.clone()
-    dm.sample_euler(ds.shape, ds.table, z_eager, sigmas, ws, **kw)  # also warms up the side stream
+    dm.sample_euler(ds.shape, ds.table, z_eager, sigmas, ws, **kw)
     torch.cuda.synchronize()
     z_static = z0.clone()
     graph = torch.cuda.CUDAGraph()
