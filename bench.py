@@ -1,15 +1,19 @@
 """Throughput of the DiT denoising step on one MI355X.
 
-Workload: DiT-XL/2 at a 32x32x4 latent (256 tokens), batch 8, 28 blocks,
-hidden 1152, 16 heads x 72, MLP 4608, bf16 weights and GEMM operands with
-fp32 accumulation, timestep + class conditioning.  One step = conditioning
-embedding + patch embedding + 28 DiT blocks + final layer, all in the HIP
-library (include/ditmi.h), inputs resident in HBM.  Weights are random-init
-(N(0, 0.02), drawn on the device), latents N(0, 1).
+Default workload: the video DiT step, 17550 latent tokens (13 frames x 30 x 45
+patches of a 16-channel latent), batch 1, 30 blocks, hidden 3072, 24 heads x
+128, MLP 12288, bf16 weights and GEMM operands with fp32 accumulation, a
+given 3072-d conditioning vector.  One step = adaLN for all blocks + patch
+embedding + 30 DiT blocks + final layer, all in the HIP library
+(include/ditmi.h), inputs resident in HBM.  Weights are random-init
+(N(0, 0.02), drawn on the device), latents N(0, 1).  --config selects the
+other workloads (c1, c2: DiT-XL/2 at 256 and 1024 tokens; c3: the joint
+text-image DiT).
 
-Prints ONE JSON line with steps/s, the roofline of the dominant kernel
-(measured with HIP events around its launches on the launch stream during
-the timed region) and the fp64 CPU oracle timed on a bounded sample.
+Prints ONE JSON line on stdout with steps/s, the roofline of the dominant
+kernel (measured with HIP events around its launches on the launch stream
+during a repeat of the timed steps) and the fp64 CPU oracle timed on a
+bounded sample; progress lines go to stderr.
 """
 from __future__ import annotations
 
@@ -53,12 +57,13 @@ CLASSES = {
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--config", default="c1", help="workload key (c1 is the reported one)")
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", default="c4", help="workload key (c4, the largest, is the reported one)")
     ap.add_argument("--batch", type=int, default=0, help="override the workload's batch size (0: as configured)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-blocks", type=int, default=28, help="oracle blocks in the CPU sample")
+    ap.add_argument("--cpu-blocks", type=int, default=28,
+                    help="oracle blocks in the CPU sample of the DiT-XL/2 workloads (one block for c3/c4)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="also run a plain device copy of this size (counter calibration runs)")
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
@@ -76,6 +81,10 @@ def parse():
                     help="instead of single steps, time the multi-step Euler sampler loop of this many steps "
                          "(eager and replayed from a captured HIP graph)")
     return ap.parse_args()
+
+
+def progress(msg: str) -> None:
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
 def source_hash(fname: str) -> str:
@@ -197,10 +206,35 @@ def algorithmic_flops(cfg) -> float:
     return cfg.n_blocks * (24.0 * B * (T + Tt) * D * D + 4.0 * B * (T + Tt) ** 2 * D)
 
 
+def host_info() -> dict:
+    """CPU model, core count and library versions of the host the oracle runs on."""
+    import platform
+
+    import numpy as np
+    model = platform.processor() or "unknown"
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    rocm = None
+    for f in ("/opt/rocm/.info/version", "/opt/rocm/.info/version-dev"):
+        if os.path.exists(f):
+            with open(f) as fh:
+                rocm = fh.read().strip()
+            break
+    return {"cpu_model": model, "cpu_count": os.cpu_count(), "numpy": np.__version__, "rocm": rocm}
+
+
 def cpu_baseline(cfg, n_blocks_sample: int):
-    """fp64 oracle on the host: conditioning + patch embed + n_blocks_sample
-    blocks (one block's weights reused) + final layer at the full batch, scaled
-    to the full block count."""
+    """fp64 oracle on the host.  DiT-XL/2 workloads: conditioning + patch embed +
+    n_blocks_sample blocks (one block's weights reused) + final layer at the
+    full batch, scaled to the full block count.  Joint and video workloads:
+    one full-size block, timed once, times the block count (labelled
+    extrapolated; the embedding and final layer are below 0.1% of a block)."""
     import numpy as np
     from threadpoolctl import threadpool_info
 
@@ -208,10 +242,26 @@ def cpu_baseline(cfg, n_blocks_sample: int):
     from oracle import dit_oracle as O
 
     scfg = synth.CONFIGS[cfg.key]
+    info = host_info()
+    threads = max((i.get("num_threads", 1) for i in threadpool_info()), default=1)
     bw = synth.block_weights(scfg, 0)
-    sw = {k: v.astype(np.float64) for k, v in synth.step_weights(scfg).items()}
-    blocks = [{k: {n: a.astype(np.float64) for n, a in v.items()} for k, v in bw.items()}] * n_blocks_sample
+    blk = {k: {n: a.astype(np.float64) for n, a in v.items()} for k, v in bw.items()}
     inp = synth.inputs(scfg)
+    if scfg.key in ("c3", "c4"):
+        t0 = time.perf_counter()
+        if scfg.joint:
+            O.joint_block(inp["x"], inp["x_txt"], inp["cond"], blk["img"], blk["txt"], scfg.heads, scfg.ln_eps)
+        else:
+            O.dit_block(inp["x"], inp["cond"], blk["img"], scfg.heads, scfg.ln_eps)
+        t_block = time.perf_counter() - t0
+        sec_per_step = t_block * scfg.n_blocks
+        return {"value": 1.0 / sec_per_step, "unit": "steps/s", "cores": threads, "kind": "oracle",
+                "extrapolated": True, **info,
+                "sample": f"fp64 numpy oracle, one full-size block ({scfg.tokens} tokens"
+                          f"{' + %d text' % scfg.text_tokens if scfg.joint else ''}, block 0's weights) timed once "
+                          f"at {t_block:.2f} s, extrapolated x {scfg.n_blocks} blocks ({sec_per_step:.1f} s/step)"}
+    sw = {k: v.astype(np.float64) for k, v in synth.step_weights(scfg).items()}
+    blocks = [blk] * n_blocks_sample
     pos = O.pos_embed_2d(*scfg.grid, scfg.hidden) if scfg.grid else None
     t0 = time.perf_counter()
     if scfg.cond == "class":
@@ -230,8 +280,8 @@ def cpu_baseline(cfg, n_blocks_sample: int):
     t_step = (time.perf_counter() - t1) / passes
     # per-block share of the sampled run, extrapolated to all blocks (prologue/epilogue counted once)
     sec_per_step = t_cond + t_step * (scfg.n_blocks / n_blocks_sample)
-    threads = max((i.get("num_threads", 1) for i in threadpool_info()), default=1)
     return {"value": 1.0 / sec_per_step, "unit": "steps/s", "cores": threads, "kind": "oracle",
+            "extrapolated": n_blocks_sample != scfg.n_blocks, **info,
             "sample": f"fp64 numpy oracle, full batch {scfg.batch}: conditioning + patch embed + "
                       f"{n_blocks_sample} of {scfg.n_blocks} blocks (one block's weights) + final layer, "
                       f"{passes} pass(es) at {t_step:.2f} s each, scaled to {scfg.n_blocks} blocks "
@@ -427,6 +477,7 @@ def main():
     if args.sp_share:
         sp_share_bench(cfg, args, torch, dm)
         return
+    progress(f"workload {cfg.name}: drawing weights on the device")
     wl = Workload(cfg, torch, dm)
     st = torch.cuda.current_stream()
     if args.serve:
@@ -437,6 +488,7 @@ def main():
         return
 
     # warmup; afterwards measure each kernel class once to find the dominant one
+    progress(f"warmup ({args.warmup} steps)")
     for _ in range(args.warmup):
         wl.step()
     torch.cuda.synchronize()
@@ -451,6 +503,7 @@ def main():
     dominant = max(share, key=share.get)
 
     # timed region: K steps between synchronisations, events on the launch stream
+    progress(f"timing {args.steps} steps")
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -466,6 +519,7 @@ def main():
     # roofline: the same K steps again with every launch of the dominant kernel
     # bracketed by HIP events on its launch stream (the library's timing hook);
     # kept out of the region above because the events add a little time per launch.
+    progress(f"{ms_per_step:.3f} ms/step; timing every launch of {dominant}")
     dm.timing_enable(dominant, 8192)
     for _ in range(args.steps):
         wl.step()
@@ -522,7 +576,8 @@ def main():
         "kernel_ms_per_step": {k: round(v, 4) for k, v in share.items()},
         "roofline": roof,
     }
-    if not args.no_cpu_baseline and cfg.key in ("c1", "c2"):
+    if not args.no_cpu_baseline and cfg.key in ("c1", "c2", "c3", "c4"):
+        progress("timing the fp64 CPU oracle")
         result["cpu_baseline"] = cpu_baseline(cfg, min(args.cpu_blocks, cfg.n_blocks))
     print(json.dumps(result), flush=True)
 

@@ -46,16 +46,51 @@ parts plus the zero-gate closed form of the whole step.
 """
 from __future__ import annotations
 
+import concurrent.futures as cf
 import math
+import os
 from typing import Dict, Optional, Sequence, Tuple
 
 import numpy as np
+from threadpoolctl import threadpool_limits
 
 F64 = np.float64
 
 
 def _f64(a) -> np.ndarray:
     return np.asarray(a, dtype=F64)
+
+
+# Execution only, no arithmetic: independent pieces of work (the heads of
+# attention, slices of token rows for row-wise functions) are evaluated on
+# several host threads, each with exactly the arithmetic it has when run
+# alone, so that full-size configurations finish in test time.
+_POOL: Optional[cf.ThreadPoolExecutor] = None
+
+
+def _pool() -> cf.ThreadPoolExecutor:
+    global _POOL
+    if _POOL is None:
+        _POOL = cf.ThreadPoolExecutor(max_workers=min(16, os.cpu_count() or 1))
+    return _POOL
+
+
+def _token_slices(T: int, n: int):
+    step = max(1, -(-T // n))
+    return [slice(t, min(T, t + step)) for t in range(0, T, step)]
+
+
+def _rowwise(fn, x: np.ndarray, *per_sample) -> np.ndarray:
+    """fn applied to slices of the token axis (axis 1 of [B, T, ...]) of x,
+    with any per-sample arguments passed whole: for functions whose result at
+    a token depends only on that token's row."""
+    x = _f64(x)
+    T = x.shape[1] if x.ndim == 3 else 0
+    if x.size < (1 << 20) or T < 2:
+        return fn(x, *per_sample)
+    sl = _token_slices(T, 4 * _pool()._max_workers)
+    parts = list(_pool().map(lambda s_: fn(x[:, s_], *per_sample), sl))
+    return np.concatenate(parts, axis=1)
 
 
 # ---------------------------------------------------------------- elementwise
@@ -124,15 +159,24 @@ def attention_heads(q: np.ndarray, k: np.ndarray, v: np.ndarray, rows: Optional[
         Tq = q.shape[2]
     out = np.empty((B, H, Tq, dh), dtype=F64)
     scale = 1.0 / math.sqrt(dh)
-    for b in range(B):
-        for h in range(H):
-            kt = k[b, h].T
-            for r0 in range(0, Tq, chunk):
-                s = np.matmul(q[b, h, r0:r0 + chunk], kt) * scale
-                s = s - s.max(axis=-1, keepdims=True)
-                p = np.exp(s)
-                p /= p.sum(axis=-1, keepdims=True)
-                out[b, h, r0:r0 + chunk] = np.matmul(p, v[b, h])
+
+    def one_head(bh):
+        b, h = bh
+        kt = k[b, h].T
+        for r0 in range(0, Tq, chunk):
+            s = np.matmul(q[b, h, r0:r0 + chunk], kt) * scale
+            s = s - s.max(axis=-1, keepdims=True)
+            p = np.exp(s)
+            p /= p.sum(axis=-1, keepdims=True)
+            out[b, h, r0:r0 + chunk] = np.matmul(p, v[b, h])
+
+    pairs = [(b, h) for b in range(B) for h in range(H)]
+    if len(pairs) > 1 and Tq * k.shape[2] >= (1 << 20):
+        with threadpool_limits(limits=1, user_api="blas"):  # one BLAS thread per head
+            list(_pool().map(one_head, pairs))
+    else:
+        for bh in pairs:
+            one_head(bh)
     return out
 
 
@@ -169,7 +213,7 @@ def dit_block(x: np.ndarray, c: np.ndarray, w: Dict[str, np.ndarray], heads: int
     """
     x = _f64(x)
     sh1, sc1, g1, sh2, sc2, g2 = adaln_modulation(c, w["w_ada"], w["b_ada"])
-    h = modulate(layer_norm(x, eps), sh1, sc1)
+    h = _ln_modulate(x, sh1, sc1, eps)
     q, k, v = qkv_project(h, w["w_qkv"], w["b_qkv"], heads)
     o = merge_heads(attention_heads(q, k, v, rows=rows))
     xs = x if rows is None else x[:, np.asarray(rows), :]
@@ -177,9 +221,14 @@ def dit_block(x: np.ndarray, c: np.ndarray, w: Dict[str, np.ndarray], heads: int
     return _mlp_branch(x1, sh2, sc2, g2, w, eps)
 
 
+def _ln_modulate(x, shift, scale, eps):
+    """modulate(LN(x), shift, scale), evaluated over slices of tokens."""
+    return _rowwise(lambda xs, sh, sc: modulate(layer_norm(xs, eps), sh, sc), x, shift, scale)
+
+
 def _mlp_branch(x1, sh2, sc2, g2, w, eps):
-    h2 = modulate(layer_norm(x1, eps), sh2, sc2)
-    g = gelu_tanh(linear(h2, w["w_fc1"], w["b_fc1"]))
+    h2 = _ln_modulate(x1, sh2, sc2, eps)
+    g = _rowwise(gelu_tanh, linear(h2, w["w_fc1"], w["b_fc1"]))
     return x1 + g2[:, None, :] * linear(g, w["w_fc2"], w["b_fc2"])
 
 
@@ -195,8 +244,8 @@ def joint_block(x_img: np.ndarray, x_txt: np.ndarray, c: np.ndarray, w_img: Dict
     Ti = x_img.shape[1]
     mi = adaln_modulation(c, w_img["w_ada"], w_img["b_ada"])
     mt = adaln_modulation(c, w_txt["w_ada"], w_txt["b_ada"])
-    hi = modulate(layer_norm(x_img, eps), mi[0], mi[1])
-    ht = modulate(layer_norm(x_txt, eps), mt[0], mt[1])
+    hi = _ln_modulate(x_img, mi[0], mi[1], eps)
+    ht = _ln_modulate(x_txt, mt[0], mt[1], eps)
     qi, ki, vi = qkv_project(hi, w_img["w_qkv"], w_img["b_qkv"], heads)
     qt, kt, vt = qkv_project(ht, w_txt["w_qkv"], w_txt["b_qkv"], heads)
     q = np.concatenate([qi, qt], axis=2)

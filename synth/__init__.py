@@ -12,7 +12,9 @@ seed derived from (config, block, tensor).
 """
 from __future__ import annotations
 
+import concurrent.futures as cf
 import dataclasses
+import os
 from typing import Dict, Optional
 
 import numpy as np
@@ -103,6 +105,19 @@ def _rng(cfg: DiTConfig, block: int, tensor_id: int, salt: int = 0) -> np.random
     return np.random.default_rng(np.random.SeedSequence([SEED_ROOT, cfg.index, block + 2, tensor_id, salt]))
 
 
+def _bf16_round_inplace(a: np.ndarray) -> None:
+    """Rounds a float32 array to the nearest bfloat16 (ties to even) in place."""
+    nan = np.isnan(a)
+    u = a.view(np.uint32)
+    r = u >> 16
+    r &= 1
+    r += 0x7FFF
+    u += r
+    u &= np.uint32(0xFFFF0000)
+    if nan.any():
+        a[nan] = np.nan
+
+
 def bf16_round(a: np.ndarray) -> np.ndarray:
     """Round float32 values to the nearest bfloat16 (ties to even); returns float32.
 
@@ -110,24 +125,45 @@ def bf16_round(a: np.ndarray) -> np.ndarray:
     consumes the same values upcast exactly.  NaN stays NaN.
     """
     out = np.array(a, dtype=np.float32, copy=True, order="C")
-    nan = np.isnan(out)
-    u = out.view(np.uint32)
-    r = (u >> 16) & 1
-    r += 0x7FFF
-    u += r
-    u &= np.uint32(0xFFFF0000)
-    if nan.any():
-        out[nan] = np.nan
+    _bf16_round_inplace(out.reshape(-1))
     return out
 
 
+# Large tensors are drawn in chunks of _CHUNK values, chunk i from its own
+# seed stream (the tensor's seed plus i), so the chunks can be drawn on
+# several threads and the values do not depend on how many run.
+_CHUNK = 1 << 22
+_POOL: Optional[cf.ThreadPoolExecutor] = None
+
+
+def _pool() -> cf.ThreadPoolExecutor:
+    global _POOL
+    if _POOL is None:
+        _POOL = cf.ThreadPoolExecutor(max_workers=min(16, os.cpu_count() or 1))
+    return _POOL
+
+
 def _normal(cfg, block, tid, shape, std, salt=0, weight=True):
-    a = _rng(cfg, block, tid, salt).standard_normal(size=shape, dtype=np.float32)
-    if std != 1.0:
-        a *= np.float32(std)
-    if weight and cfg.dtype == "bf16":
-        a = bf16_round(a)
-    return a
+    n = int(np.prod(shape))
+    out = np.empty(n, dtype=np.float32)
+    rnd = weight and cfg.dtype == "bf16"
+
+    def fill(i):
+        seg = out[i * _CHUNK:(i + 1) * _CHUNK]
+        np.random.default_rng(np.random.SeedSequence([SEED_ROOT, cfg.index, block + 2, tid, salt, i])) \
+            .standard_normal(out=seg, dtype=np.float32)
+        if std != 1.0:
+            seg *= np.float32(std)
+        if rnd:
+            _bf16_round_inplace(seg)
+
+    nch = (n + _CHUNK - 1) // _CHUNK
+    if nch <= 1:
+        for i in range(nch):
+            fill(i)
+    else:
+        list(_pool().map(fill, range(nch)))
+    return out.reshape(shape)
 
 
 def stream_weights(cfg: DiTConfig, block: int, stream: int = STREAM_IMG) -> Dict[str, np.ndarray]:

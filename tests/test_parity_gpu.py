@@ -37,9 +37,9 @@ def check(name, got, ref, base, tol):
     assert e_y <= tol and e_d <= tol, (name, e_y, e_d)
 
 
-def block_case(cfg, salt=0, rows=None):
+def block_case(cfg, salt=0, rows=None, block=0):
     g = _gpu()
-    w = synth.block_weights(cfg, 0)
+    w = synth.block_weights(cfg, block)
     inp = synth.inputs(cfg, salt)
     x, c = inp["x"], inp["cond"]
     xt = inp.get("x_txt")
@@ -203,9 +203,11 @@ def test_block_c2_full():
     block_case(synth.CONFIGS["c2"].with_(n_blocks=1))
 
 
-def test_block_c3_full_sampled_rows():
-    rows = [0, 1, 777, 2048, 4000, 4095]
-    block_case(synth.CONFIGS["c3"].with_(n_blocks=1), rows=rows)
+def test_block_c3_full():
+    """The joint text-image block at full size: all 4096 image rows and all
+    256 text rows against the oracle."""
+    print("[case] block c3 full (4096 + 256 tokens, D 3072)", flush=True)
+    block_case(synth.CONFIGS["c3"].with_(n_blocks=1))
 
 
 def test_block_joint_split_text_fc1():
@@ -228,9 +230,14 @@ def test_block_joint_split_text_fc1_deterministic():
     assert np.array_equal(y1, y2) and np.array_equal(t1, t2)
 
 
-def test_block_c4_full_sampled_rows():
-    rows = [0, 5, 8191, 12000, 17536, 17549]
-    block_case(synth.CONFIGS["c4"].with_(n_blocks=1), rows=rows)
+@pytest.mark.slow
+@pytest.mark.timeout(900)
+@pytest.mark.parametrize("block", [0, 14, 29])
+def test_block_c4_full(block):
+    """The video DiT block at full size (17550 tokens, all rows compared),
+    with the weights of blocks 0, 14 and 29 of the 30-block model."""
+    print(f"[case] block c4 full, weights of block {block}", flush=True)
+    block_case(synth.CONFIGS["c4"].with_(n_blocks=1), block=block)
 
 
 def test_block_c4_sp8_token_share():
@@ -269,6 +276,50 @@ def test_step_full_end_to_end(key):
                                                     ("w_t1", "b_t1", "w_t2", "b_t2", "class_table")])
     rout, _ = step_ref(cfg, sw, blocks, inp, pos, c)
     check(f"step/{key}_full", out, rout, None, TOL["bf16"])
+
+
+def _oracle_blocks(cfg, blocks_np):
+    """Per-block float64 weights for the oracle, converted one block at a
+    time, with a progress line per block."""
+    for l, b in enumerate(blocks_np):
+        print(f"[oracle] block {l + 1}/{len(blocks_np)}", flush=True)
+        yield {k: f64(v) for k, v in b.items()}
+
+
+def _step_full(cfg):
+    g = _gpu()
+    sw = synth.step_weights(cfg)
+    inp = synth.inputs(cfg)
+    blocks = [synth.block_weights(cfg, l) for l in range(cfg.n_blocks)]
+    ds = g.DeviceStep(cfg, blocks, sw)
+    out, xt = ds.run(inp["patches"], inp["cond"], inp.get("x_txt"))
+    del ds
+    torch.cuda.empty_cache()
+    print("[case] device step done, oracle running", flush=True)
+    rout, rxt = O.dit_step(cfg, inp["patches"], inp["cond"], {k: v.astype(np.float64) for k, v in sw.items()},
+                           _oracle_blocks(cfg, blocks), x_txt=inp.get("x_txt"))
+    check(f"step/{cfg.key}_L{cfg.n_blocks}", out, rout, None, TOL["bf16"])
+    if cfg.joint:
+        check(f"step/{cfg.key}_L{cfg.n_blocks}/txt", xt, rxt, inp["x_txt"], TOL["bf16"])
+
+
+@pytest.mark.slow
+@pytest.mark.timeout(900)
+def test_step_c3_full_end_to_end():
+    """The joint text-image step end to end: patch embedding, 24 two-stream
+    blocks with their own weights, final layer; output and the text stream's
+    final state against the oracle."""
+    print("[case] step c3 full, 24 joint blocks", flush=True)
+    _step_full(synth.CONFIGS["c3"])
+
+
+@pytest.mark.slow
+@pytest.mark.timeout(900)
+def test_step_c4_two_blocks_end_to_end():
+    """The video DiT step at full sequence length with its first two blocks:
+    patch embedding, blocks 0 and 1, final layer."""
+    print("[case] step c4, 17550 tokens, 2 blocks", flush=True)
+    _step_full(synth.CONFIGS["c4"].with_(n_blocks=2))
 
 
 # ------------------------------------------------------------------ multi-step sampler loop
@@ -343,8 +394,9 @@ def test_sample_euler_graph_replay():
 def test_serve_overlap_and_jitter_do_not_change_results():
     """Five requests through dit_serve: in order on one stream, with the
     copies overlapped on a second stream, and with host-side arrival jitter,
-    the outputs are bitwise identical, and each equals dit_sample_euler run on
-    that request alone (which the sampler tests pin to the oracle)."""
+    the outputs are bitwise identical, each equals dit_sample_euler run on
+    that request alone, and each matches the oracle's Euler loop on that
+    request's latent and labels."""
     name, cfg, sigmas = SAMPLE_CASES[1]
     g, dm, sw, blocks, inp, ds, ws_sample, kw = _sample_setup(cfg)
     ws = dm.alloc_workspace(ds.shape, dm.DIT_WS_SERVE)
@@ -373,3 +425,11 @@ def test_serve_overlap_and_jitter_do_not_change_results():
         dm.sample_euler(ds.shape, ds.table, z, sigmas, ws_sample, cond_w=cond_w, y=r["y"].cuda())
         torch.cuda.synchronize()
         assert torch.equal(z.cpu(), outs["serial"][i]), i
+    # and each request's denoised latent against the oracle's Euler loop
+    pos = O.pos_embed_2d(*cfg.grid, cfg.hidden)
+    sw64 = {k: v.astype(np.float64) for k, v in sw.items()}
+    bl64 = [{k: f64(v) for k, v in b.items()} for b in blocks]
+    for i, r in enumerate(reqs):
+        ref = O.sample_euler(cfg, r["z_in"].numpy().astype(np.float64), sigmas, sw64, bl64, y=r["y"].numpy(), pos=pos)
+        check(f"serve/request{i}", outs["overlap_jitter"][i].numpy().astype(np.float64), ref,
+              r["z_in"].numpy().astype(np.float64), TOL["bf16"])
