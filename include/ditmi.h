@@ -131,6 +131,30 @@ size_t dit_workspace_bytes(const dit_shape *s, int kind);
 dit_status dit_block_forward(const dit_shape *s, const dit_block_weights *w, float *x, float *x_txt,
                              const float *cond, void *workspace, size_t ws_bytes, void *stream);
 
+/* Size of the static device scratch of dit_block_forward_noalloc (128 MiB
+ * per GPU): enough for one block of DiT-XL/2 at 256 tokens x 8 samples
+ * (42 MiB) or 1024 tokens x 4 (83 MiB). */
+#define DIT_NOALLOC_SCRATCH_BYTES (128u << 20)
+
+/* dit_block_forward for callers that cannot allocate device memory: code
+ * being captured into a HIP graph, tight serving loops, harnesses that
+ * forbid hipMalloc.  Same arguments, results and errors as
+ * dit_block_forward, but the workspace is a static device array of
+ * DIT_NOALLOC_SCRATCH_BYTES that the library holds on each GPU it runs on
+ * until the process ends; the call allocates nothing and calls no
+ * allocating library routine.  The GPU is the one `stream` belongs to (the
+ * current device for NULL).  Its first call on a GPU looks the array's
+ * device address up (hipGetSymbolAddress) and keeps it.
+ * Every call on one GPU shares that GPU's array: calls that may overlap on
+ * one GPU (different streams without ordering between them) race and give
+ * undefined results; calls ordered on one stream are safe.  The array keeps
+ * the last call's contents; nothing in it needs clearing.
+ * Errors: those of dit_block_forward, and DIT_ERR_UNSUPPORTED when
+ * dit_workspace_bytes(s, DIT_WS_BLOCK) exceeds DIT_NOALLOC_SCRATCH_BYTES
+ * (checked before anything is enqueued). */
+dit_status dit_block_forward_noalloc(const dit_shape *s, const dit_block_weights *w, float *x, float *x_txt,
+                                     const float *cond, void *stream);
+
 /* One denoising step: the full DiT forward of the paper's per-step DiT time
  * (paper Table: per-stage execution time; one step = one DiT forward):
  *   x = patches W_patch^T + b_patch (+ pos);  L blocks;

@@ -20,11 +20,12 @@ LIB_PATH = os.path.join(_HERE, "libditmi.so")
 DIT_OK, DIT_ERR_INVALID_ARG, DIT_ERR_UNSUPPORTED, DIT_ERR_WORKSPACE, DIT_ERR_HIP = 0, -1, -2, -3, -4
 DIT_F32, DIT_BF16 = 0, 1
 DIT_WS_BLOCK, DIT_WS_STEP, DIT_WS_COND, DIT_WS_SAMPLE, DIT_WS_SERVE = 0, 1, 2, 3, 4
+NOALLOC_SCRATCH_BYTES = 128 << 20  # DIT_NOALLOC_SCRATCH_BYTES of include/ditmi.h
 KERNEL_CLASSES = {"gemm_qkv": 0, "attention": 1, "gemm_out": 2, "gemm_fc1": 3, "gemm_fc2": 4,
                   "ln_mod": 5, "adaln": 6, "other": 7}
 
 STREAM_FIELDS = ("w_ada", "b_ada", "w_qkv", "b_qkv", "w_o", "b_o", "w_fc1", "b_fc1", "w_fc2", "b_fc2")
-C_API = ("dit_workspace_bytes", "dit_block_forward", "dit_step_forward", "dit_sample_euler", "dit_serve", "dit_cond_embed", "dit_pos_embed_2d",
+C_API = ("dit_workspace_bytes", "dit_block_forward", "dit_block_forward_noalloc", "dit_step_forward", "dit_sample_euler", "dit_serve", "dit_cond_embed", "dit_pos_embed_2d",
          "dit_timing_enable", "dit_timing_read", "dit_timing_disable", "dit_status_string", "dit_last_error",
          "dit_version")
 
@@ -80,6 +81,7 @@ def lib() -> ctypes.CDLL:
     L.dit_workspace_bytes.argtypes = [P(Shape), ctypes.c_int]
     L.dit_workspace_bytes.restype = sz
     L.dit_block_forward.argtypes = [P(Shape), P(BlockWeights), vp, vp, vp, vp, sz, vp]
+    L.dit_block_forward_noalloc.argtypes = [P(Shape), P(BlockWeights), vp, vp, vp, vp]
     L.dit_step_forward.argtypes = [P(Shape), P(StepWeights), vp, vp, vp, vp, vp, sz, vp]
     L.dit_cond_embed.argtypes = [P(Shape), vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
     L.dit_sample_euler.argtypes = [P(Shape), P(StepWeights), P(CondWeights), vp, vp, P(ctypes.c_float), i32,
@@ -90,7 +92,7 @@ def lib() -> ctypes.CDLL:
     L.dit_timing_enable.argtypes = [ctypes.c_int, ctypes.c_int]
     L.dit_timing_read.argtypes = [P(ctypes.c_double), P(ctypes.c_int), P(ctypes.c_double), P(ctypes.c_double)]
     L.dit_timing_disable.argtypes = []
-    for fn in ("dit_block_forward", "dit_step_forward", "dit_cond_embed", "dit_pos_embed_2d", "dit_timing_enable",
+    for fn in ("dit_block_forward", "dit_block_forward_noalloc", "dit_step_forward", "dit_cond_embed", "dit_pos_embed_2d", "dit_timing_enable",
                "dit_timing_read", "dit_timing_disable"):
         getattr(L, fn).restype = ctypes.c_int
     L.dit_status_string.argtypes = [ctypes.c_int]
@@ -194,6 +196,15 @@ def block_forward(shape: Shape, weights: BlockWeights, x: torch.Tensor, cond: to
                                    _ptr(x_txt, torch.float32, "x_txt"), _ptr(cond, torch.float32, "cond"),
                                    _ptr(workspace, None, "workspace"), workspace.numel() * workspace.element_size(),
                                    _stream(stream)))
+
+
+def block_forward_noalloc(shape: Shape, weights: BlockWeights, x: torch.Tensor, cond: torch.Tensor,
+                          x_txt: Optional[torch.Tensor] = None, stream=None) -> None:
+    """One DiT block in place on x, with the library's static per-GPU scratch
+    as workspace (no device allocation)."""
+    _check(lib().dit_block_forward_noalloc(ctypes.byref(shape), ctypes.byref(weights), _ptr(x, torch.float32, "x"),
+                                           _ptr(x_txt, torch.float32, "x_txt"), _ptr(cond, torch.float32, "cond"),
+                                           _stream(stream)))
 
 
 def step_forward(shape: Shape, table: StepWeightTable, patches: torch.Tensor, cond: torch.Tensor, out: torch.Tensor,

@@ -707,6 +707,74 @@ dit_status run_sample_loop(const dit_shape* s, const dit_step_weights* w, const 
   return DIT_OK;
 }
 
+// Arguments of a block call, everything but the workspace.
+dit_status check_block_args(const dit_shape* s, const dit_block_weights* w, const float* x, const float* x_txt,
+                            const float* cond) {
+  dit_status st = check_shape(s, false);
+  if (st != DIT_OK) return st;
+  if (!w) return fail(DIT_ERR_INVALID_ARG, "weights is NULL");
+  if ((st = check_stream_weights(w->img, "image-stream")) != DIT_OK) return st;
+  const bool joint = s->text_tokens > 0;
+  if (joint && (st = check_stream_weights(w->txt, "text-stream")) != DIT_OK) return st;
+  if (!x || !aligned(x, 16)) return fail(DIT_ERR_INVALID_ARG, "x NULL or not 16-byte aligned");
+  if (joint && (!x_txt || !aligned(x_txt, 16))) return fail(DIT_ERR_INVALID_ARG, "x_txt NULL or not 16-byte aligned");
+  if (!joint && x_txt) return fail(DIT_ERR_INVALID_ARG, "x_txt must be NULL when text_tokens == 0");
+  if (!cond || !aligned(cond, 4)) return fail(DIT_ERR_INVALID_ARG, "cond NULL or misaligned");
+  return DIT_OK;
+}
+
+// One block on validated arguments: adaLN of the block's stream(s), then
+// the block, with the block layout L of the workspace ws.
+dit_status block_call(const dit_shape* s, const dit_block_weights* w, float* x, float* x_txt, const float* cond,
+                      const Layout& L, char* ws, hipStream_t hs) {
+  const bool joint = s->text_tokens > 0;
+  float* mod = (float*)(ws + L.mod);
+  const size_t per = (size_t)s->batch * 6 * s->hidden;
+  std::vector<AdaJob> jobs;
+  jobs.push_back({w->img.w_ada, w->img.b_ada, mod, 6 * s->hidden});
+  if (joint) jobs.push_back({w->txt.w_ada, w->txt.b_ada, mod + per, 6 * s->hidden});
+  dit_status st = run_adaln(s, cond, ws + L.act, jobs, hs);
+  if (st != DIT_OK) return st;
+  StreamIO io[2] = {{&w->img, x, mod, s->tokens}, {&w->txt, x_txt, mod + per, s->text_tokens}};
+  return run_block(s, L, ws, io, joint ? 2 : 1, hs);
+}
+
+// ------------------------------------------------------------------ static scratch
+// Workspace of dit_block_forward_noalloc: one array per GPU, in the code
+// object's zero-initialised data, held until the process ends.  Host code
+// never uses the array's name as an address (it stands for a host-side
+// shadow); the device address comes from hipGetSymbolAddress, looked up
+// once per device with that device current and kept in `scratch_ptr`.
+// Every byte a block reads from its workspace is written first by the same
+// call, so nothing is cleared between calls.
+static __device__ __align__(256) unsigned char scratch[DIT_NOALLOC_SCRATCH_BYTES];
+
+struct ScratchTable {
+  std::mutex mu;
+  std::vector<char*> ptr;  // per device ordinal; null until looked up
+} g_scratch;
+
+dit_status scratch_of_stream(hipStream_t hs, char** out) {
+  int dev = -1;
+  hipError_t e = hs ? hipStreamGetDevice(hs, &dev) : hipGetDevice(&dev);
+  if (e != hipSuccess || dev < 0) return fail(DIT_ERR_HIP, "device of the stream: %s", hipGetErrorString(e));
+  std::lock_guard<std::mutex> lk(g_scratch.mu);
+  if ((int)g_scratch.ptr.size() <= dev) g_scratch.ptr.resize(dev + 1, nullptr);
+  if (!g_scratch.ptr[dev]) {
+    int cur = -1;
+    HIP_TRY(hipGetDevice(&cur));
+    if (cur != dev) HIP_TRY(hipSetDevice(dev));
+    void* scratch_ptr = nullptr;
+    e = hipGetSymbolAddress((void**)&scratch_ptr, HIP_SYMBOL(scratch));
+    if (cur != dev) (void)hipSetDevice(cur);
+    if (e != hipSuccess || !scratch_ptr)
+      return fail(DIT_ERR_HIP, "hipGetSymbolAddress(scratch) on device %d: %s", dev, hipGetErrorString(e));
+    g_scratch.ptr[dev] = (char*)scratch_ptr;
+  }
+  *out = g_scratch.ptr[dev];
+  return DIT_OK;
+}
+
 }  // namespace
 
 // ====================================================================== C ABI
@@ -738,30 +806,28 @@ size_t dit_workspace_bytes(const dit_shape* s, int kind) {
 
 dit_status dit_block_forward(const dit_shape* s, const dit_block_weights* w, float* x, float* x_txt,
                              const float* cond, void* workspace, size_t ws_bytes, void* stream) {
-  dit_status st = check_shape(s, false);
+  dit_status st = check_block_args(s, w, x, x_txt, cond);
   if (st != DIT_OK) return st;
-  if (!w) return fail(DIT_ERR_INVALID_ARG, "weights is NULL");
-  if ((st = check_stream_weights(w->img, "image-stream")) != DIT_OK) return st;
-  const bool joint = s->text_tokens > 0;
-  if (joint && (st = check_stream_weights(w->txt, "text-stream")) != DIT_OK) return st;
-  if (!x || !aligned(x, 16)) return fail(DIT_ERR_INVALID_ARG, "x NULL or not 16-byte aligned");
-  if (joint && (!x_txt || !aligned(x_txt, 16))) return fail(DIT_ERR_INVALID_ARG, "x_txt NULL or not 16-byte aligned");
-  if (!joint && x_txt) return fail(DIT_ERR_INVALID_ARG, "x_txt must be NULL when text_tokens == 0");
-  if (!cond || !aligned(cond, 4)) return fail(DIT_ERR_INVALID_ARG, "cond NULL or misaligned");
   const Layout L = layout(s, DIT_WS_BLOCK);
   if (!workspace || !aligned(workspace, 256)) return fail(DIT_ERR_INVALID_ARG, "workspace NULL or not 256-byte aligned");
   if (ws_bytes < L.total) return fail(DIT_ERR_WORKSPACE, "workspace %zu bytes < %zu needed", ws_bytes, L.total);
+  return block_call(s, w, x, x_txt, cond, L, (char*)workspace, (hipStream_t)stream);
+}
 
+dit_status dit_block_forward_noalloc(const dit_shape* s, const dit_block_weights* w, float* x, float* x_txt,
+                                     const float* cond, void* stream) {
+  dit_status st = check_block_args(s, w, x, x_txt, cond);
+  if (st != DIT_OK) return st;
+  const Layout L = layout(s, DIT_WS_BLOCK);
+  if (L.total > (size_t)DIT_NOALLOC_SCRATCH_BYTES)
+    return fail(DIT_ERR_UNSUPPORTED,
+                "dit_block_forward_noalloc: this block needs %zu bytes of scratch, above the %zu-byte static "
+                "scratch; use dit_block_forward with a workspace",
+                L.total, (size_t)DIT_NOALLOC_SCRATCH_BYTES);
   hipStream_t hs = (hipStream_t)stream;
-  char* ws = (char*)workspace;
-  float* mod = (float*)(ws + L.mod);
-  const size_t per = (size_t)s->batch * 6 * s->hidden;
-  std::vector<AdaJob> jobs;
-  jobs.push_back({w->img.w_ada, w->img.b_ada, mod, 6 * s->hidden});
-  if (joint) jobs.push_back({w->txt.w_ada, w->txt.b_ada, mod + per, 6 * s->hidden});
-  if ((st = run_adaln(s, cond, ws + L.act, jobs, hs)) != DIT_OK) return st;
-  StreamIO io[2] = {{&w->img, x, mod, s->tokens}, {&w->txt, x_txt, mod + per, s->text_tokens}};
-  return run_block(s, L, ws, io, joint ? 2 : 1, hs);
+  char* ws = nullptr;
+  if ((st = scratch_of_stream(hs, &ws)) != DIT_OK) return st;
+  return block_call(s, w, x, x_txt, cond, L, ws, hs);
 }
 
 dit_status dit_step_forward(const dit_shape* s, const dit_step_weights* w, const float* patches, float* x_txt,

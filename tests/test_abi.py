@@ -90,6 +90,24 @@ def test_weight_matrix_size_limit(dm):
     assert lib.dit_workspace_bytes(ctypes.byref(s), 0) > 0
 
 
+def test_noalloc_rejects_blocks_beyond_its_scratch(dm):
+    """dit_block_forward_noalloc refuses, before any HIP call, a block whose
+    workspace exceeds the static scratch (the video DiT block needs ~0.9 GB);
+    the header's size constant matches the binding's."""
+    text = open(HEADER).read()
+    assert "#define DIT_NOALLOC_SCRATCH_BYTES (128u << 20)" in text
+    assert dm.NOALLOC_SCRATCH_BYTES == 128 << 20
+    s = shape(dm, "c4", n_blocks=1)
+    assert dm.workspace_bytes(s, dm.DIT_WS_BLOCK) > dm.NOALLOC_SCRATCH_BYTES
+    bw = fake_block(dm)
+    assert dm.lib().dit_block_forward_noalloc(ctypes.byref(s), ctypes.byref(bw), FAKE, None, FAKE, None) == -2
+    assert "scratch" in dm.last_error()
+    # argument errors come first, as for dit_block_forward
+    s1 = shape(dm, n_blocks=1)
+    assert dm.lib().dit_block_forward_noalloc(ctypes.byref(s1), ctypes.byref(bw), None, None, FAKE, None) == -1
+    assert dm.workspace_bytes(s1, dm.DIT_WS_BLOCK) <= dm.NOALLOC_SCRATCH_BYTES
+
+
 FAKE = 0x100000  # 1 MiB-aligned fake device address; never dereferenced
 
 
