@@ -246,7 +246,7 @@ static double tile_rounds(long tiles) { return (double)((tiles + 255) / 256); }
 // k-ranges (each at least 4 slices) whose S-times-shorter units fill that
 // round, and a reduction adds the ranges.  Returns S, or 0 for no split.
 static int tail_split(const GemmProb* p, int np, int epi, int bm, int bn, size_t part_cap) {
-  if (np != 2 || epi != EPI_GELU || part_cap == 0) return 0;
+  if (np != 2 || (epi != EPI_GELU && epi != EPI_RESID && epi != EPI_RESID2) || part_cap == 0) return 0;
   const long t0 = (long)((p[0].M + bm - 1) / bm) * ((p[0].N + bn - 1) / bn);
   const long t1 = (long)((p[1].M + bm - 1) / bm) * ((p[1].N + bn - 1) / bn);
   if (t0 < 256 || t0 % 256 != 0 || t1 == 0 || 2 * t1 > 256) return 0;
@@ -337,12 +337,52 @@ int choose_tile(const GemmProb* p, int np, int epi, size_t part_cap, int* split)
   return cfg;
 }
 
+// Row tail: a single problem of whole rounds of 256-row tiles plus a short
+// last round (the video DiT's fc2 and output projection at 17550 tokens:
+// 828 tiles of 256 x 256 = 3 rounds + 60 tiles) is cut after the last row
+// tile that completes a round; the rows after it become the second problem
+// of the tail schedule, whose tiles run as k-range units in the last round.
+// Applies where the sample index of a row stays valid in the second part
+// (one sample, or a cut at a sample boundary).  Returns the split (0: none;
+// the problem is then unchanged).
+static int row_tail(GemmArgs& a, int epi, int bm, int bn, size_t part_cap) {
+  if (a.nprob != 1 || bm != 256 || (epi != EPI_GELU && epi != EPI_RESID && epi != EPI_RESID2)) return 0;
+  const GemmProb& p = a.p[0];
+  const long tm = (p.M + bm - 1) / bm, tn = (p.N + bn - 1) / bn;
+  if (tm * tn <= 256 || (tm * tn) % 256 == 0) return 0;
+  long m0 = 0;
+  for (long m = tm - 1; m >= 1 && !m0; --m)
+    if ((m * tn) % 256 == 0) m0 = m;
+  if (!m0) return 0;
+  const long M0 = m0 * bm, rpb = p.rows_per_batch;
+  if (p.M > rpb && M0 % rpb != 0) return 0;
+  GemmProb two[2] = {p, p};
+  two[0].M = (int)M0;
+  two[1].M = (int)(p.M - M0);
+  const int S = tail_split(two, 2, epi, bm, bn, part_cap);
+  if (!S || tail_rounds(m0 * tn, S) >= tile_rounds(tm * tn)) return 0;
+  GemmProb& q = two[1];
+  q.A = (const uint16_t*)p.A + M0 * p.K;  // bf16 elements
+  q.rows_per_batch = (int)rpb;
+  if (epi == EPI_GELU) {
+    q.out = (uint16_t*)p.out + M0 * p.N;
+  } else {
+    q.resid = p.resid + M0 * p.N;
+    q.gate = p.gate + (M0 / rpb) * p.gate_stride;
+  }
+  a.p[0] = two[0];
+  a.p[1] = q;
+  a.nprob = 2;
+  return S;
+}
+
 hipError_t run_gemm(Gemm& G, int dtype, hipStream_t st) {
   GemmArgs& a = G.a;
   int bm = 64, bn = 64, tcfg = 0, split = 0;
   if (dtype == DIT_BF16) {
     tcfg = choose_tile(a.p, a.nprob, G.epi, G.part_cap, &split);
     gemm_tile_dims(tcfg, &bm, &bn);
+    if (!split) split = row_tail(a, G.epi, bm, bn, G.part_cap);
   }
   int tiles = 0;
   for (int i = 0; i < a.nprob; ++i) {

@@ -220,6 +220,21 @@ def test_block_joint_split_text_fc1():
     block_case(cfg, rows=[0, 1, 1000, 2047])
 
 
+def test_block_row_tail_split():
+    """One sample of 8200 tokens at hidden 2048: the output projection and
+    fc2 are 528 tiles of 256 x 128, two whole rounds plus 16 tiles; rows from
+    8192 on run as k-range units in the last round and their partials are
+    reduced with the bias, gate and residual update.  Compared in full, and
+    bitwise between two runs."""
+    cfg = synth.CONFIGS["c4"].with_(tokens=8200, hidden=2048, heads=16, head_dim=128, mlp_hidden=8192, n_blocks=1)
+    print("[case] row tail split, 8200 tokens, hidden 2048", flush=True)
+    block_case(cfg)
+    g = _gpu()
+    inp = synth.inputs(cfg)
+    (y1, _), (y2, _) = g.run_block(cfg, synth.block_weights(cfg, 0), inp["x"], inp["cond"], repeat=2)
+    assert np.array_equal(y1, y2)
+
+
 def test_block_joint_split_text_fc1_deterministic():
     """The split ranges are added in a fixed order: two runs agree bitwise."""
     g = _gpu()
