@@ -70,6 +70,11 @@ def parse():
                     help="no GPU work: turn two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE) of this "
                          "command with --copy-probe-mib into profiles/<kernel>_<workload>_traffic.json")
     ap.add_argument("--kernel-class", default=None, help="kernel class for --summarize-pmc")
+    ap.add_argument("--summarize-profile", nargs=6,
+                    metavar=("CONFIG", "TRACE_DIR", "PMC_DIR", "FETCH_DIR", "WRITE_DIR", "BENCH_JSON"),
+                    help="no GPU work: write profiles/counters_<config>.md (and per-class traffic records) from a "
+                         "kernel-trace run, a --pmc run of PMC_COUNTERS, FETCH_SIZE and WRITE_SIZE runs and the "
+                         "bench line of the trace run")
     ap.add_argument("--serve", type=int, default=0,
                     help="time N requests through dit_serve (copies in order vs overlapped on a second "
                          "stream) with --sample-steps (default 1) Euler steps each")
@@ -145,6 +150,139 @@ def summarize_pmc(fetch_dir, write_dir, kclass, workload, copy_mib):
     with open(path, "w") as fh:
         json.dump(out, fh, indent=1)
     print(json.dumps(out))
+
+
+PMC_COUNTERS = ("MfmaUtil LdsUtil LDSBankConflict VALUBusy SQ_INSTS_VALU_MFMA_MOPS_BF16 "
+                "SQ_VALU_MFMA_COEXEC_CYCLES GRBM_GUI_ACTIVE")
+
+
+def summarize_profile(key, trace_dir, pmc_dir, fetch_dir, write_dir, bench_json, copy_mib):
+    """profiles/counters_<key>.md: per kernel class, the kernel-trace average
+    (from trace_dir), the counters of one --pmc pass (MFMA and LDS
+    utilisation, VALU busy, MFMA ops, GRBM active cycles as the clock) and the
+    HBM bytes of the FETCH_SIZE / WRITE_SIZE passes scaled by a plain copy of
+    copy_mib MiB; algorithmic work per launch comes from the bench line of
+    the trace run.  Also writes profiles/<class>_<key>_traffic.json for the
+    bench's roofline.traffic."""
+    import csv
+    import glob
+    import re
+    import statistics
+
+    import synth
+    cfg = synth.CONFIGS[key]
+    with open(bench_json) as fh:
+        bench = json.loads([l for l in fh if l.startswith("{")][-1])
+    alg = bench["kernel_algorithmic_per_launch"]
+    stats = []
+    for f in glob.glob(os.path.join(trace_dir, "**", "*kernel_stats.csv"), recursive=True):
+        with open(f) as fh:
+            stats += list(csv.DictReader(fh))
+    pmc = _pmc_rows(pmc_dir)
+    fetch = [r for r in _pmc_rows(fetch_dir) if r["Counter_Name"] == "FETCH_SIZE"]
+    write = [r for r in _pmc_rows(write_dir) if r["Counter_Name"] == "WRITE_SIZE"]
+
+    def copy_factor(rows):
+        c = [float(r["Counter_Value"]) * 1024 for r in rows
+             if "elementwise" in r["Kernel_Name"] or "copy" in r["Kernel_Name"].lower()]
+        return max(c) / (copy_mib * (1 << 20)), max(c)
+
+    f_fac, f_probe = copy_factor(fetch)
+    w_fac, w_probe = copy_factor(write)
+    out_rows = []
+    for k, (rx, src) in CLASSES.items():
+        pat = re.compile(rx)
+        st = [r for r in stats if pat.search(r["Name"])]
+        if not st:
+            continue
+        calls = sum(int(r["Calls"]) for r in st)
+        avg_us = sum(float(r["TotalDurationNs"]) for r in st) / calls / 1e3
+        names = sorted({r["Name"].split("(")[0].replace("void ditmi::", "") for r in st})
+        a = alg.get(k, {})
+        fl, by = a.get("flops", 0.0), a.get("bytes", 0.0)
+
+        def per_dispatch(rows, counter):
+            vals = [float(r["Counter_Value"]) for r in rows if r["Counter_Name"] == counter and pat.search(r["Kernel_Name"])]
+            return statistics.mean(vals) if vals else None
+
+        def mean_dur_ns(rows):
+            d = {}
+            for r in rows:
+                if pat.search(r["Kernel_Name"]):
+                    d[r["Dispatch_Id"]] = int(r["End_Timestamp"]) - int(r["Start_Timestamp"])
+            return statistics.mean(d.values()) if d else None
+
+        row = {"class": k, "kernels": names, "calls": calls, "trace_avg_us": avg_us, "alg_flops": fl, "alg_bytes": by}
+        for c in ("MfmaUtil", "LdsUtil", "LDSBankConflict", "VALUBusy", "SQ_INSTS_VALU_MFMA_MOPS_BF16",
+                  "SQ_VALU_MFMA_COEXEC_CYCLES", "GRBM_GUI_ACTIVE"):
+            row[c] = per_dispatch(pmc, c)
+        dur = mean_dur_ns(pmc)
+        row["pmc_dispatch_us"] = dur / 1e3 if dur else None
+        # GRBM_GUI_ACTIVE is summed over the 8 XCDs
+        row["clock_ghz"] = row["GRBM_GUI_ACTIVE"] / 8 / dur if dur and row["GRBM_GUI_ACTIVE"] else None
+        fb, wb = per_dispatch(fetch, "FETCH_SIZE"), per_dispatch(write, "WRITE_SIZE")
+        row["fetch_bytes"] = fb * 1024 / f_fac if fb is not None else None
+        row["write_bytes"] = wb * 1024 / w_fac if wb is not None else None
+        out_rows.append(row)
+        if row["fetch_bytes"] is not None and row["write_bytes"] is not None:
+            rec = {"kernel_class": k, "workload": key, "source_hash": source_hash(src),
+                   "fetch_bytes_per_launch": row["fetch_bytes"], "write_bytes_per_launch": row["write_bytes"],
+                   "hbm_bytes_per_launch": row["fetch_bytes"] + row["write_bytes"], "fetch_factor": f_fac,
+                   "write_factor": w_fac, "copy_probe_mib": copy_mib}
+            with open(os.path.join(PROFILES, f"{k}_{key}_traffic.json"), "w") as fh:
+                json.dump(rec, fh, indent=1)
+
+    def f(v, fmt):
+        return "-" if v is None else format(v, fmt)
+
+    cmds = [
+        f"rocprofv3 --kernel-trace --stats -f csv -d {trace_dir} -o t -- python -u bench.py --config {key} "
+        f"--no-cpu-baseline > {bench_json}",
+        f"rocprofv3 --kernel-trace --pmc {PMC_COUNTERS} -f csv -d {pmc_dir} -o a -- python -u bench.py --config {key} "
+        f"--no-cpu-baseline --steps 2 --warmup 1",
+        f"rocprofv3 --pmc FETCH_SIZE -f csv -d {fetch_dir} -o f -- python -u bench.py --config {key} --no-cpu-baseline "
+        f"--steps 2 --warmup 1 --copy-probe-mib {copy_mib}",
+        f"rocprofv3 --pmc WRITE_SIZE -f csv -d {write_dir} -o w -- python -u bench.py --config {key} --no-cpu-baseline "
+        f"--steps 2 --warmup 1 --copy-probe-mib {copy_mib}",
+        f"python bench.py --summarize-profile {key} {trace_dir} {pmc_dir} {fetch_dir} {write_dir} {bench_json} "
+        f"--copy-probe-mib {copy_mib}",
+    ]
+    L = [f"# Kernel counters: {cfg.name}", "",
+         f"Workload {key}: batch {cfg.batch}, {cfg.tokens} tokens"
+         f"{' + %d text tokens' % cfg.text_tokens if cfg.joint else ''}, hidden {cfg.hidden}, "
+         f"{cfg.heads} x {cfg.head_dim} heads, MLP {cfg.mlp_hidden}, {cfg.n_blocks} blocks, bf16.  "
+         f"Step: {bench['ms_per_step']} ms ({bench['value']} steps/s) in the trace run.", "",
+         "Commands (repo root, one MI355X):", "", "```", *cmds, "```", "",
+         "Columns: trace average per launch; algorithmic TFLOP/s and % of the 2.5 PFLOP/s dense bf16 peak; "
+         "MfmaUtil = MFMA-busy cycles / (GRBM active cycles x SIMDs); MFMA ops / algorithmic flops "
+         "(MOPS x 512; above 1 where MFMA tiles are padded, e.g. head_dim 72 -> 80); clock = GRBM active "
+         "cycles per XCD / dispatch time in the counter pass; LDS = LdsUtil and LDSBankConflict (% of "
+         "active cycles); VALU = VALUBusy; HBM = FETCH_SIZE and WRITE_SIZE per launch, each divided by "
+         f"what the counter reads for a {copy_mib} MiB device copy (fetch factor {f_fac:.3f}, write factor "
+         f"{w_fac:.3f}), against the algorithmic bytes of the launch.", "",
+         "| class | kernel | launches | avg us | TFLOP/s | % peak | MfmaUtil % | MFMA/alg | clock GHz | LDS util % | "
+         "LDS conflict % | VALU % | fetch MB | write MB | HBM GB/s | alg MB | HBM/alg |",
+         "|" + "---|" * 17]
+    for r in out_rows:
+        tf = r["alg_flops"] / (r["trace_avg_us"] * 1e-6) / 1e12 if r["alg_flops"] else None
+        hbm = (r["fetch_bytes"] or 0) + (r["write_bytes"] or 0) if r["fetch_bytes"] is not None else None
+        mops = r["SQ_INSTS_VALU_MFMA_MOPS_BF16"]
+        L.append("| " + " | ".join([
+            r["class"], "<br>".join(f"`{n}`" for n in r["kernels"]), str(r["calls"]), f(r["trace_avg_us"], ".2f"),
+            f(tf, ".1f"), f(tf / PEAK_BF16_TFLOPS * 100 if tf else None, ".1f"), f(r["MfmaUtil"], ".1f"),
+            f(mops * 512 / r["alg_flops"] if mops and r["alg_flops"] else None, ".3f"), f(r["clock_ghz"], ".2f"),
+            f(r["LdsUtil"], ".1f"), f(r["LDSBankConflict"], ".2f"), f(r["VALUBusy"], ".1f"),
+            f(r["fetch_bytes"] / 1e6 if r["fetch_bytes"] is not None else None, ".1f"),
+            f(r["write_bytes"] / 1e6 if r["write_bytes"] is not None else None, ".1f"),
+            f(hbm / (r["trace_avg_us"] * 1e-6) / 1e9 if hbm else None, ".0f"),
+            f(r["alg_bytes"] / 1e6 if r["alg_bytes"] else None, ".1f"),
+            f(hbm / r["alg_bytes"] if hbm and r["alg_bytes"] else None, ".2f")]) + " |")
+    L += ["", f"Copy probe: FETCH_SIZE {f_probe / 2**20:.1f} MiB, WRITE_SIZE {w_probe / 2**20:.1f} MiB for a "
+              f"{copy_mib} MiB copy.", ""]
+    path = os.path.join(PROFILES, f"counters_{key}.md")
+    with open(path, "w") as fh:
+        fh.write("\n".join(L))
+    print(path)
 
 
 class Workload:
@@ -453,6 +591,9 @@ def sp_share_bench(cfg, args, torch, dm):
 
 def main():
     args = parse()
+    if args.summarize_profile:
+        summarize_profile(*args.summarize_profile, args.copy_probe_mib or 256)
+        return
     if args.summarize_pmc:
         import synth
         summarize_pmc(args.summarize_pmc[0], args.summarize_pmc[1], args.kernel_class,
@@ -492,7 +633,7 @@ def main():
     for _ in range(args.warmup):
         wl.step()
     torch.cuda.synchronize()
-    share = {}
+    share, alg = {}, {}
     for k in CLASSES:
         dm.timing_enable(k, 4096)
         wl.step()
@@ -500,6 +641,7 @@ def main():
         ms, n, fl, by = dm.timing_read()
         dm.timing_disable()
         share[k] = ms
+        alg[k] = {"launches_per_step": n, "flops": fl / max(n, 1), "bytes": by / max(n, 1)}
     dominant = max(share, key=share.get)
 
     # timed region: K steps between synchronisations, events on the launch stream
@@ -574,6 +716,7 @@ def main():
         "step_frac_of_bf16_peak": round(flops / (ms_per_step * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
         "wall_s_timed": round(wall, 3),
         "kernel_ms_per_step": {k: round(v, 4) for k, v in share.items()},
+        "kernel_algorithmic_per_launch": alg,
         "roofline": roof,
     }
     if not args.no_cpu_baseline and cfg.key in ("c1", "c2", "c3", "c4"):

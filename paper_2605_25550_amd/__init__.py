@@ -15,7 +15,9 @@ from typing import Dict, Optional, Sequence
 import torch
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libditmi.so")
+# DITMI_LIB names another build of the same library (a sanitizer build, or a
+# variant being measured); the default is the in-tree build.
+LIB_PATH = os.environ.get("DITMI_LIB") or os.path.join(_HERE, "libditmi.so")
 
 DIT_OK, DIT_ERR_INVALID_ARG, DIT_ERR_UNSUPPORTED, DIT_ERR_WORKSPACE, DIT_ERR_HIP = 0, -1, -2, -3, -4
 DIT_F32, DIT_BF16 = 0, 1

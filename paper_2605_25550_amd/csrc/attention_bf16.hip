@@ -441,17 +441,16 @@ __global__ __launch_bounds__(NW * 64, WPC) void attn_bf16_pipe_kernel(AttnArgs a
   f32x16 oacc[C::DT];
 #pragma unroll
   for (int t = 0; t < C::DT; ++t) oacc[t] = f32x16{};
+  // Accumulator operand of each tile's first QK^T MFMAs: -m_run in every
+  // element (zero with FOLD, where the product subtracts m_run itself).  The
+  // MFMA reads it as its C operand and writes S^T elsewhere, so the block is
+  // set only when m_run moves, not copied into the accumulators every tile.
+  f32x16 sinit = f32x16{};
+  // bf16 ones, for the row sums of the bf16 probabilities by dot2 (the same
+  // values the PV product multiplies)
+  const bf16x2v ones2 = {(__bf16)1.0f, (__bf16)1.0f};
 
-  // S^T of one key tile minus m_run; s_mask sets keys past the end to -inf.
-  auto s_init = [&](f32x16 (&s)[2]) {
-#pragma unroll
-    for (int kt = 0; kt < 2; ++kt) {
-      f32x16 init;
-#pragma unroll
-      for (int e = 0; e < 16; ++e) init[e] = FOLD ? 0.f : -m_run;
-      s[kt] = init;
-    }
-  };
+  // s_mask sets the scores of keys past the end to -inf.
   auto s_mask = [&](int kv0, f32x16 (&s)[2]) {
     if (kv0 + C::BKV > Tj) {
 #pragma unroll
@@ -463,13 +462,12 @@ __global__ __launch_bounds__(NW * 64, WPC) void attn_bf16_pipe_kernel(AttnArgs a
   };
   auto qk = [&](int tile, f32x16 (&s)[2]) {
     const unsigned char* sl = smem + (tile % ST) * C::SLOT;
-    s_init(s);
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
       for (int st = 0; st < C::KS; ++st) {
         const bf16x8 kf = *(const bf16x8*)(sl + kt * 32 * C::KROW + k_off[st]);
-        s[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[st], s[kt], 0, 0, 0);
+        s[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[st], st == 0 ? sinit : s[kt], 0, 0, 0);
       }
   };
   auto rowmax = [&](const f32x16 (&s)[2]) {
@@ -515,6 +513,9 @@ __global__ __launch_bounds__(NW * 64, WPC) void attn_bf16_pipe_kernel(AttnArgs a
       for (int kt = 0; kt < 2; ++kt) scur[kt] -= delta;
       m_run = m_new;
       if (FOLD && g == C::QG) qf[C::QS][C::QE] = __builtin_bit_cast(__bf16, f2bf(-m_run));
+      if (!FOLD)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) sinit[e] = -m_run;
       first = false;
     }
     // Softmax of tile j interleaved by hand with the QK^T MFMAs of tile j+1
@@ -529,29 +530,24 @@ __global__ __launch_bounds__(NW * 64, WPC) void attn_bf16_pipe_kernel(AttnArgs a
     {
       const int tn = min(j + 1, nkv - 1), kvn = tn * C::BKV;
       const unsigned char* sln = smem + (tn % ST) * C::SLOT;
-      s_init(snext);
       constexpr int NQ = 2 * C::KS;  // QK^T MFMAs per tile; MFMA i: half i % 2, k-step i / 2
       auto kread = [&](int i) { return *(const bf16x8*)(sln + (i & 1) * 32 * C::KROW + k_off[i >> 1]); };
       bf16x8 kf[3];
       kf[0] = kread(0);
       kf[1] = kread(1);
-      float lsum = 0.f;
 #pragma unroll
       for (int i = 0; i < NQ; ++i) {
         if (i + 2 < NQ) kf[(i + 2) % 3] = kread(i + 2);
-        snext[i & 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[i % 3], qf[i >> 1], snext[i & 1], 0, 0, 0);
+        snext[i & 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[i % 3], qf[i >> 1], i < 2 ? sinit : snext[i & 1],
+                                                               0, 0, 0);
 #pragma unroll
         for (int t = 0; t < IPW; ++t)
           if (i == 1 + t * (NQ - 1) / IPW) issue_one(j + ST - 1, t);
 #pragma unroll
-        for (int e = i * 32 / NQ; e < (i + 1) * 32 / NQ; ++e) {
-          const float p = __builtin_amdgcn_exp2f(scur[e >> 4][e & 15]);
-          scur[e >> 4][e & 15] = p;
-          if (!FOLD) lsum += p;
-        }
+        for (int e = i * 32 / NQ; e < (i + 1) * 32 / NQ; ++e)
+          scur[e >> 4][e & 15] = __builtin_amdgcn_exp2f(scur[e >> 4][e & 15]);
         __builtin_amdgcn_sched_barrier(0);
       }
-      if (!FOLD) l_run += lsum;
     }
     u32x4 pw[4];
 #pragma unroll
@@ -574,7 +570,7 @@ __global__ __launch_bounds__(NW * 64, WPC) void attn_bf16_pipe_kernel(AttnArgs a
       u32x4 vf[3];
       vf[0] = vread(0);
       vf[1] = vread(1);
-      float m = -INFINITY;
+      float m = -INFINITY, lsum = 0.f;
 #pragma unroll
       for (int i = 0; i < NP; ++i) {
         if (i + 2 < NP) vf[(i + 2) % 3] = vread(i + 2);
@@ -583,9 +579,22 @@ __global__ __launch_bounds__(NW * 64, WPC) void attn_bf16_pipe_kernel(AttnArgs a
                                                                   oacc[i % C::DT], 0, 0, 0);
 #pragma unroll
         for (int e = i * 32 / NP; e < (i + 1) * 32 / NP; ++e) m = fmaxf(m, snext[e >> 4][e & 15]);
+        // row sum of the tile's bf16 probabilities: 16 packed pairs, spread
+        // one or more per MFMA
+        if (!FOLD)
+#pragma unroll
+          for (int w = i * 16 / NP; w < (i + 1) * 16 / NP; ++w)
+          {
+            // (the element is copied out first: a bit_cast of a vector
+            // element reference reads element 0 with this compiler)
+            const uint32_t pair = pw[w >> 2][w & 3];
+            lsum = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2v, pair), ones2, lsum, false);
+            asm volatile("" : "+v"(lsum));  // keeps the sum here, between the MFMAs
+          }
         __builtin_amdgcn_sched_barrier(0);
       }
       mcur = max_halves(m);
+      if (!FOLD) l_run += lsum;
     }
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt) scur[kt] = snext[kt];
