@@ -59,5 +59,50 @@ def build(extra: list[str] | None = None, jobs: int = 8) -> str:
     return LIB
 
 
+# Host-code sanitizers for the CPU tests of the C ABI: the host side
+# (ditmi.cpp: validation, workspace layout, tile planning, launch sequencing)
+# is rebuilt with AddressSanitizer and UndefinedBehaviorSanitizer; the kernel
+# objects are the regular ones (device code is never sanitized).  The library
+# is loaded into a process that preloads the ASan runtime (sanitizer_runtime()).
+SAN_FLAGS = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
+             "-Xarch_host", "-fno-sanitize-recover=undefined", "-Xarch_host", "-fno-omit-frame-pointer",
+             "-Xarch_host", "-g"]
+
+
+def sanitizer_runtime() -> str:
+    """Path of clang's shared ASan runtime (to preload)."""
+    import glob
+    root = os.path.dirname(os.path.dirname(os.path.realpath(hipcc())))
+    for pat in ("llvm/lib/clang/*/lib/linux/libclang_rt.asan-x86_64.so",
+                "lib/llvm/lib/clang/*/lib/linux/libclang_rt.asan-x86_64.so"):
+        hits = sorted(glob.glob(os.path.join(root, pat)))
+        if hits:
+            return hits[-1]
+    raise RuntimeError("clang's ASan runtime was not found")
+
+
+def build_sanitized(out_dir: str) -> str:
+    """libditmi.so with the host code under ASan + UBSan, in out_dir."""
+    os.makedirs(OBJDIR, exist_ok=True)
+    os.makedirs(out_dir, exist_ok=True)
+    kernels = [s for s in SOURCES if s != "ditmi.cpp"]
+    objs = [os.path.join(OBJDIR, os.path.splitext(s)[0] + ".o") for s in kernels]
+    missing = [s for s, o in zip(kernels, objs) if not os.path.exists(o)]
+    with cf.ThreadPoolExecutor(max_workers=8) as ex:
+        list(ex.map(lambda s: _compile(s, []), missing))
+    host = os.path.join(out_dir, "ditmi_san.o")
+    cmd = [hipcc(), f"--offload-arch={ARCH}", "-O1", "-fPIC", "-std=c++17", "-I", INCLUDE, "-I", CSRC, *DEVICE_FLAGS,
+           *SAN_FLAGS, "-c", os.path.join(CSRC, "ditmi.cpp"), "-o", host]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"sanitized compile failed:\n{r.stdout}{r.stderr}")
+    lib = os.path.join(out_dir, "libditmi.so")
+    cmd = [hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", *SAN_FLAGS, host, *objs, "-o", lib]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"sanitized link failed:\n{r.stdout}{r.stderr}")
+    return lib
+
+
 if __name__ == "__main__":
     print(build())
