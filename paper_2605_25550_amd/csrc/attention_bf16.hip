@@ -340,14 +340,20 @@ __global__ __launch_bounds__(NW * 64, WPC) void attn_bf16_pipe_kernel(AttnArgs a
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int g = lane >> 5, r32 = lane & 31;
-  const int b = blockIdx.z, h = blockIdx.y;
+  // Work item (query block, head, sample), query block fastest, taken in
+  // contiguous ranges per XCD: the workgroups an XCD runs at once are query
+  // blocks of the same head and share its K and V tiles in that XCD's L2.
   const int Tj = a.Tj, Tjp = a.Tj_pad;
-  const long bh = (long)b * a.H + h;
+  const int nqb = (Tj + NW * 32 - 1) / (NW * 32);
+  const int item = xcd_remap(blockIdx.x, nqb * a.H * a.B);
+  const int qb = item % nqb, bh_i = item / nqb;
+  const int h = bh_i % a.H, b = bh_i / a.H;
+  const long bh = bh_i;
   const bf16_t* __restrict__ qp = (const bf16_t*)a.q + bh * Tj * C::DHP;
   const bf16_t* __restrict__ kp = (const bf16_t*)a.k + bh * Tj * C::DHP;
   const bf16_t* __restrict__ vp = (const bf16_t*)a.v + bh * DH * (long)Tjp;
   const unsigned lds0 = __builtin_amdgcn_readfirstlane(lds_address(smem));
-  const int q0 = blockIdx.x * (NW * 32) + wave * 32;  // first query of this wave
+  const int q0 = qb * (NW * 32) + wave * 32;  // first query of this wave
   const int nkv = (Tj + C::BKV - 1) / C::BKV;
 
   // DMA of one tile (layout as in the kernel above) into slot tile % ST.  The
@@ -644,8 +650,9 @@ hipError_t launch_attn_bf16(const AttnArgs& a, int head_dim, hipStream_t st) {
   const bool wide = items >= 256 || (items >= 128 && a.Tj >= 2048);
   const int nw = wide ? 8 : 4;
   dim3 grid((a.Tj + nw * 32 - 1) / (nw * 32), a.H, a.B), block(nw * 64);
+  dim3 grid1(grid.x * grid.y * grid.z);  // the pipelined kernel maps a 1-D grid to its items
 #define ATTN_LAUNCH(DHV)                                                                   \
-  if (wide) hipLaunchKernelGGL((attn_bf16_pipe_kernel<DHV, 8>), grid, block, 0, st, a);   \
+  if (wide) hipLaunchKernelGGL((attn_bf16_pipe_kernel<DHV, 8>), grid1, block, 0, st, a);  \
   else hipLaunchKernelGGL((attn_bf16_dma_kernel<DHV, 4, 1>), grid, block, 0, st, a);
   switch (head_dim) {
     case 64: ATTN_LAUNCH(64) break;

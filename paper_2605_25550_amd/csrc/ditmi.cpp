@@ -10,6 +10,7 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <algorithm>
 #include <chrono>
 #include <mutex>
 #include <thread>
@@ -376,6 +377,30 @@ static int row_tail(GemmArgs& a, int epi, int bm, int bn, size_t part_cap) {
   return S;
 }
 
+// Height (in M-tiles) of the tile groups of the GEMM's tile order.  An XCD
+// runs a contiguous range of that order, c tiles at a time (one per
+// workgroup slot of its 32 CUs, or its whole share of a smaller grid); such
+// a range spans about g M-tiles and c / g N-tiles, so it reads
+// g BM rows of A and (c / g) BN rows of W per k-slice from the XCD's L2.
+// The height with the least of that (ties: the taller) is used.  DiT-XL/2's
+// QKV projection at 256 tokens x 8 (8 x 27 tiles of 256 x 128, 27 per XCD):
+// 4 M-tiles x 7 N-tiles per XCD instead of 8 x 3.4.
+static int group_height(int tiles_m, int tiles_n, int bm, int bn, int tcfg) {
+  const long tiles = (long)tiles_m * tiles_n;
+  const int per_cu = tcfg == TILE_128x128 || tcfg == TILE_64x128 || tcfg == TILE_64x144_1 ? 2
+                     : tcfg == TILE_64x128_S2                                             ? 3
+                                                                                          : 1;
+  const long c = std::min<long>(32L * per_cu, (tiles + 7) / 8);
+  int best = 8;
+  double best_cost = -1;
+  for (int g = 16; g >= 1; g /= 2) {
+    const int gm = std::min(g, tiles_m);
+    const double cost = (double)gm * bm + (double)((c + gm - 1) / gm) * bn;
+    if (best_cost < 0 || cost < best_cost) best = gm, best_cost = cost;
+  }
+  return best < 1 ? 1 : best;
+}
+
 hipError_t run_gemm(Gemm& G, int dtype, hipStream_t st) {
   GemmArgs& a = G.a;
   int bm = 64, bn = 64, tcfg = 0, split = 0;
@@ -389,6 +414,7 @@ hipError_t run_gemm(Gemm& G, int dtype, hipStream_t st) {
     GemmProb& p = a.p[i];
     p.tiles_m = (p.M + bm - 1) / bm;
     p.tiles_n = (p.N + bn - 1) / bn;
+    p.group_m = group_height(p.tiles_m, p.tiles_n, bm, bn, dtype == DIT_BF16 ? tcfg : -1);
     p.tile_begin = tiles;
     p.ksplit = 0;
     p.part = nullptr;

@@ -361,13 +361,16 @@ hipError_t launch_cond_embed(int B, int D, const float* t, const int32_t* y, con
   return hipGetLastError();
 }
 
-// ---------------------------------------------------------------- patch embedding
-// x[row][n] = sum_p z[row][p] W[n][p] + bias[n] (+ pos[row % T][n]); one
-// workgroup per token row, the patch vector staged in LDS.
+// Patch embedding x = z W^T + b (+ pos), fp32 accumulation in the order
+// b, p = 0 .. P-1, then pos.
+//
+// Up to 16 channels (patch_row_kernel): one workgroup per token row, the
+// patch vector in LDS, each lane a column.
 template <typename WT>
-__global__ __launch_bounds__(256) void patch_embed_kernel(int T, int P, int D, const float* z, const WT* w,
-                                                          const WT* bias, const float* pos, float* x) {
-  __shared__ float zs[256];
+__global__ __launch_bounds__(256) void patch_row_kernel(int T, int P, int D, const float* __restrict__ z,
+                                                        const WT* __restrict__ w, const WT* __restrict__ bias,
+                                                        const float* __restrict__ pos, float* __restrict__ x) {
+  __shared__ float zs[16];
   const int row = blockIdx.x, tid = threadIdx.x;
   if (tid < P) zs[tid] = z[(long)row * P + tid];
   __syncthreads();
@@ -381,14 +384,85 @@ __global__ __launch_bounds__(256) void patch_embed_kernel(int T, int P, int D, c
   }
 }
 
+// More channels (patch_tile_kernel): a workgroup owns 256 consecutive
+// columns and PT_ROWS rows.  Per chunk of 64 channels, the rows' latent
+// values are staged in LDS (read back as one broadcast 16-byte read per four
+// channels) and each lane holds its column's 64 weights in registers, so
+// every weight element is read once per workgroup instead of once per row.
+constexpr int PT_ROWS = 32, PT_CHUNK = 64;
+
+template <typename WT>
+__global__ __launch_bounds__(256) void patch_tile_kernel(int rows, int T, int P, int D, const float* __restrict__ z,
+                                                         const WT* __restrict__ w, const WT* __restrict__ bias,
+                                                         const float* __restrict__ pos, float* __restrict__ x) {
+  __shared__ __attribute__((aligned(16))) float zs[PT_ROWS][PT_CHUNK];
+  const int tid = threadIdx.x;
+  const int n = blockIdx.x * 256 + tid;
+  const int r0 = blockIdx.y * PT_ROWS;
+  const int nr = min(PT_ROWS, rows - r0);
+  const bool col = n < D;
+  const float b = col ? ld_as_float<WT>(bias, n) : 0.f;
+  float acc[PT_ROWS];
+#pragma unroll
+  for (int r = 0; r < PT_ROWS; ++r) acc[r] = b;
+  for (int p0 = 0; p0 < P; p0 += PT_CHUNK) {
+    const int pc = min(PT_CHUNK, P - p0);
+    __syncthreads();  // the previous chunk's reads are done
+    for (int e = tid; e < PT_ROWS * PT_CHUNK; e += 256) {
+      const int r = e / PT_CHUNK, c = e % PT_CHUNK;
+      zs[r][c] = r < nr && c < pc ? z[(long)(r0 + r) * P + p0 + c] : 0.f;
+    }
+    float wv[PT_CHUNK];
+#pragma unroll
+    for (int c = 0; c < PT_CHUNK; ++c) wv[c] = col && c < pc ? ld_as_float<WT>(w, (long)n * P + p0 + c) : 0.f;
+    __syncthreads();
+    if (pc == PT_CHUNK) {
+#pragma unroll
+      for (int r = 0; r < PT_ROWS; ++r)
+#pragma unroll
+        for (int c = 0; c < PT_CHUNK; c += 4) {
+          const f32x4 zv = *(const f32x4*)&zs[r][c];
+          acc[r] = fmaf(wv[c], zv[0], acc[r]);
+          acc[r] = fmaf(wv[c + 1], zv[1], acc[r]);
+          acc[r] = fmaf(wv[c + 2], zv[2], acc[r]);
+          acc[r] = fmaf(wv[c + 3], zv[3], acc[r]);
+        }
+    } else {  // last, partial chunk (static register indices, channels c < pc only)
+#pragma unroll
+      for (int r = 0; r < PT_ROWS; ++r)
+#pragma unroll
+        for (int c = 0; c < PT_CHUNK; ++c)
+          if (c < pc) acc[r] = fmaf(wv[c], zs[r][c], acc[r]);
+    }
+  }
+  if (!col) return;
+#pragma unroll
+  for (int r = 0; r < PT_ROWS; ++r) {
+    if (r >= nr) break;
+    const int row = r0 + r;
+    float v = acc[r];
+    if (pos) v += pos[(long)(row % T) * D + n];
+    x[(long)row * D + n] = v;
+  }
+}
+
+template <typename WT>
+static void launch_patch_embed_t(int rows, int T, int P, int D, const float* z, const WT* w, const WT* b,
+                                 const float* pos, float* x, hipStream_t st) {
+  if (P <= 16)
+    hipLaunchKernelGGL((patch_row_kernel<WT>), dim3(rows), dim3(256), 0, st, T, P, D, z, w, b, pos, x);
+  else
+    hipLaunchKernelGGL((patch_tile_kernel<WT>), dim3((D + 255) / 256, (rows + PT_ROWS - 1) / PT_ROWS), dim3(256), 0,
+                       st, rows, T, P, D, z, w, b, pos, x);
+}
+
 hipError_t launch_patch_embed(int rows, int T, int P, int D, const float* z, const void* w, const void* b,
                               const float* pos, float* x, int dtype, hipStream_t st) {
+  if (rows <= 0) return hipSuccess;
   if (dtype == 1)
-    hipLaunchKernelGGL((patch_embed_kernel<bf16_t>), dim3(rows), dim3(256), 0, st, T, P, D, z,
-                       (const bf16_t*)w, (const bf16_t*)b, pos, x);
+    launch_patch_embed_t<bf16_t>(rows, T, P, D, z, (const bf16_t*)w, (const bf16_t*)b, pos, x, st);
   else
-    hipLaunchKernelGGL((patch_embed_kernel<float>), dim3(rows), dim3(256), 0, st, T, P, D, z,
-                       (const float*)w, (const float*)b, pos, x);
+    launch_patch_embed_t<float>(rows, T, P, D, z, (const float*)w, (const float*)b, pos, x, st);
   return hipGetLastError();
 }
 

@@ -218,11 +218,14 @@ struct Epilogue {
 };
 
 // Tile `local` of problem P -> its first row and column.  Tiles are taken in
-// groups of 8 M-tiles x all N-tiles, M fastest within a group, so that
-// consecutive tiles share W columns and a group's A rows stay in one L2.
+// groups of P.group_m M-tiles x all N-tiles, M fastest within a group, so
+// that consecutive tiles share W columns and a group's A rows stay in one
+// L2; the XCDs run contiguous ranges of this order, and the host picks the
+// group height that makes the range an XCD runs at once touch the fewest
+// rows of A and W.
 template <int BM, int BN>
 __device__ __forceinline__ void tile_origin(const GemmProb& P, int local, int& m0, int& n0) {
-  const int GM = 8;
+  const int GM = max(P.group_m, 1);
   const int group_size = GM * P.tiles_n;
   const int group = local / group_size;
   const int first_m = group * GM;
@@ -504,7 +507,7 @@ __global__ __launch_bounds__(384 * KG) void gemm_bf16_144_kernel(GemmArgs args) 
   const bool second = args.nprob > 1 && tile >= args.p[1].tile_begin;
   const GemmProb P = second ? args.p[1] : args.p[0];
   const int local = tile - P.tile_begin;
-  const int GM = 8;
+  const int GM = max(P.group_m, 1);  // as tile_origin
   const int group_size = GM * P.tiles_n;
   const int group = local / group_size;
   const int first_m = group * GM;
@@ -744,7 +747,8 @@ hipError_t launch_splitk_resid(const float* part, int S, int M, int N, const voi
 void gemm_tile_dims(int tile_cfg, int* bm, int* bn) {
   switch (tile_cfg) {
     case TILE_128x128: *bm = 128; *bn = 128; break;
-    case TILE_64x144: *bm = 64; *bn = 144; break;
+    case TILE_64x144:
+    case TILE_64x144_1: *bm = 64; *bn = 144; break;
     case TILE_256x256: *bm = 256; *bn = 256; break;
     case TILE_256x128: *bm = 256; *bn = 128; break;
     case TILE_256x192: *bm = 256; *bn = 192; break;
@@ -798,6 +802,7 @@ hipError_t launch_gemm_bf16(const GemmArgs& a, int epi, int tile_cfg, hipStream_
     case TILE_64x128: return launch_tile<64, 128, 2, 2, 3>(a, epi, st);
     case TILE_64x128_S2: return launch_tile<64, 128, 2, 2, 2>(a, epi, st);
     case TILE_64x144: return launch_144(a, epi, st);
+    case TILE_64x144_1: return launch_144_kg<1>(a, epi, st);
     case TILE_256x256: return launch_tile<256, 256, 2, 4, 2>(a, epi, st);
     case TILE_256x128: return launch_tile<256, 128, 4, 2, 3>(a, epi, st);
     case TILE_256x192: return launch_tile<256, 192, 4, 2, 2>(a, epi, st);

@@ -23,6 +23,7 @@ struct GemmProb {
   const void* bias;   // [N]
   int M, N, K;
   int tiles_m, tiles_n, tile_begin;
+  int group_m;         // tile order: groups of group_m M-tiles x all N-tiles, M fastest (>= 1)
   int rows_per_batch;  // sample index b = m / rows_per_batch
   // EPI_RESID
   float* resid;
@@ -138,7 +139,9 @@ hipError_t launch_axpy_f32(float* z, const float* v, float a, long n, hipStream_
 // Tile configurations of the bf16 GEMM (BM x BN, LDS ring depth).
 enum {
   TILE_128x128 = 0, TILE_64x128 = 1, TILE_64x128_S2 = 2, TILE_64x144 = 3,
-  TILE_256x256 = 4, TILE_256x128 = 5, TILE_256x192 = 6, TILE_COUNT = 7
+  TILE_256x256 = 4, TILE_256x128 = 5, TILE_256x192 = 6,
+  TILE_64x144_1 = 7,  // 64 x 144 with one k-group of six waves (two workgroups per CU)
+  TILE_COUNT = 8
 };
 void gemm_tile_dims(int tile_cfg, int* bm, int* bn);
 
