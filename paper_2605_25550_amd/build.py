@@ -17,6 +17,7 @@ OBJDIR = os.path.join(PKG, "_build")
 ARCH = "gfx950"
 
 SOURCES = ["gemm_bf16.hip", "gemm_f32.hip", "attention_bf16.hip", "attention_f32.hip", "elementwise.hip", "ditmi.cpp"]
+PROBE = os.path.join(PKG, "gemm_probe")
 
 # Packed-fp32 instructions are disabled for every device compile.
 DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
@@ -57,6 +58,19 @@ def build(extra: list[str] | None = None, jobs: int = 8) -> str:
         raise RuntimeError(f"link failed:\n{r.stdout}{r.stderr}")
     os.replace(tmp, LIB)
     return LIB
+
+
+def build_probe() -> str:
+    """The GEMM timing probe (csrc/gemm_probe.cpp, a measurement tool linked
+    against the built library's internal launch functions)."""
+    if not os.path.exists(LIB):
+        build()
+    cmd = [hipcc(), f"--offload-arch={ARCH}", "-O2", "-std=c++17", "-I", INCLUDE, "-I", CSRC,
+           os.path.join(CSRC, "gemm_probe.cpp"), "-o", PROBE, "-L", PKG, "-lditmi", "-Wl,-rpath,$ORIGIN"]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"probe build failed:\n{r.stdout}{r.stderr}")
+    return PROBE
 
 
 # Host-code sanitizers for the CPU tests of the C ABI: the host side
@@ -105,4 +119,4 @@ def build_sanitized(out_dir: str) -> str:
 
 
 if __name__ == "__main__":
-    print(build())
+    print(build_probe() if sys.argv[1:] == ["probe"] else build())

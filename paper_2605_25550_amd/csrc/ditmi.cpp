@@ -629,7 +629,7 @@ dit_status run_adaln(const dit_shape* s, const float* cond, void* act, const std
                      hipStream_t st) {
   const size_t E = s->dtype == DIT_BF16 ? 2 : 4;
   if (s->dtype == DIT_BF16)
-    HIP_TRY(timed(DIT_K_ADALN, 0, 0, st, [&]() { return launch_silu_bf16(s->batch, s->hidden, cond, act, st); }));
+    HIP_TRY(timed(DIT_K_OTHER, 0, 0, st, [&]() { return launch_silu_bf16(s->batch, s->hidden, cond, act, st); }));
   for (size_t j0 = 0; j0 < jobs.size(); j0 += ADA_MAX_ENTRIES) {
     AdaArgs a{};
     a.cond = cond;
