@@ -345,12 +345,16 @@ __device__ __forceinline__ void gemm_mainloop(const GemmProb& P, int m0, int n0,
   bf16x8 xa[C::TM], xb[C::TN], ya[C::TM], yb[C::TN];
   GEMM_READ(xa, xb, 0, 0);
   int slot = 0;
-  for (int kt = 0; kt < KT; ++kt) {
+  // One slice.  dma1 / dma2: whether the two refills (slices kt-1+STAGES and
+  // kt+STAGES) exist, mid: both exist and slice kt+1 is not the last in
+  // flight.  The loop below runs the slices where all three hold with
+  // literal true, so the steady state has no branches around its DMAs.
+  auto iteration = [&](const int kt, const bool dma1, const bool dma2, const bool mid) __attribute__((always_inline)) {
     const int next = slot + 1 == STAGES ? 0 : slot + 1;
     const int prev = slot == 0 ? STAGES - 1 : slot - 1;  // slot of slice kt-1, refilled with kt-1+STAGES
     GEMM_READ(ya, yb, slot, 1);
     SCHED_FENCE();
-    GEMM_MFMA_DMA(xa, xb, kt >= 1 && kt - 1 + STAGES < KT, kt - 1 + STAGES, prev, H1, H2);
+    GEMM_MFMA_DMA(xa, xb, dma1, kt - 1 + STAGES, prev, H1, H2);
     SCHED_FENCE();
     GEMM_READ(xa, xb, slot, 2);
     SCHED_FENCE();
@@ -360,15 +364,24 @@ __device__ __forceinline__ void gemm_mainloop(const GemmProb& P, int m0, int n0,
     SCHED_FENCE();
     GEMM_MFMA(xa, xb);
     SCHED_FENCE();
-    if (kt + STAGES - 1 < KT) wait_vmcnt<(STAGES - 2) * C::IPW>();  // own DMA of slice kt+1 landed
+    if (mid) wait_vmcnt<(STAGES - 2) * C::IPW>();  // own DMA of slice kt+1 landed
     else wait_vmcnt<0>();
     __syncthreads();
     GEMM_READ(xa, xb, next, 0);  // past the last slice this reads stale data, unused
     SCHED_FENCE();
-    GEMM_MFMA_DMA(ya, yb, kt + STAGES < KT, kt + STAGES, slot, 0, H1);
+    GEMM_MFMA_DMA(ya, yb, dma2, kt + STAGES, slot, 0, H1);
     SCHED_FENCE();
     slot = next;
-  }
+  };
+  auto generic = [&](const int kt) __attribute__((always_inline)) {
+    iteration(kt, kt >= 1 && kt - 1 + STAGES < KT, kt + STAGES < KT, kt + STAGES - 1 < KT);
+  };
+  // slices 1 .. KT-STAGES-1 have both refills and a slice in flight behind kt+1
+  const int steady_end = KT - STAGES;
+  if (KT > 0) generic(0);
+  int kt = 1;
+  for (; kt < steady_end; ++kt) iteration(kt, true, true, true);
+  for (; kt < KT; ++kt) generic(kt);
 #undef GEMM_READ
 #undef GEMM_MFMA
 #undef GEMM_MFMA_DMA
