@@ -70,6 +70,9 @@ def parse():
                     help="no GPU work: turn two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE) of this "
                          "command with --copy-probe-mib into profiles/<kernel>_<workload>_traffic.json")
     ap.add_argument("--kernel-class", default=None, help="kernel class for --summarize-pmc")
+    ap.add_argument("--blas-ref", nargs="+", metavar="MxNxK",
+                    help="time torch.matmul (hipBLASLt, bf16, no epilogue) at these GEMM shapes, for comparison "
+                         "with paper_2605_25550_amd/gemm_probe; prints one line per shape")
     ap.add_argument("--summarize-profile", nargs=6,
                     metavar=("CONFIG", "TRACE_DIR", "PMC_DIR", "FETCH_DIR", "WRITE_DIR", "BENCH_JSON"),
                     help="no GPU work: write profiles/counters_<config>.md (and per-class traffic records) from a "
@@ -598,6 +601,28 @@ def main():
         import synth
         summarize_pmc(args.summarize_pmc[0], args.summarize_pmc[1], args.kernel_class,
                       synth.CONFIGS[args.config].key, args.copy_probe_mib or 256)
+        return
+    if args.blas_ref:
+        import torch
+        torch.cuda.set_device(0)
+        for spec in args.blas_ref:
+            M, N, K = (int(v) for v in spec.lower().split("x"))
+            a = torch.randn(M, K, device="cuda", dtype=torch.bfloat16)
+            w = torch.randn(N, K, device="cuda", dtype=torch.bfloat16)
+            for _ in range(5):
+                c = a @ w.t()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            torch.cuda.synchronize()
+            e0.record()
+            for _ in range(30):
+                c = a @ w.t()
+            e1.record()
+            torch.cuda.synchronize()
+            us = e0.elapsed_time(e1) * 1e3 / 30
+            tf = 2.0 * M * N * K / (us * 1e-6) / 1e12
+            print(f"torch.matmul bf16 {M}x{N}x{K}: {us:.2f} us  {tf:.1f} TFLOP/s  {100 * tf / PEAK_BF16_TFLOPS:.1f}%",
+                  flush=True)
+            del a, w, c
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path (run with --gpus 1)",
