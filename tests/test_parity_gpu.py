@@ -158,6 +158,14 @@ def test_cond_embed_and_pos_table():
 # ------------------------------------------------------------------ step (small)
 STEP_SMALL = [
     ("fp32_step_l2", synth.CONFIGS["c0"].with_(n_blocks=2, batch=2, tokens=64, grid=(8, 8))),
+    # patch embeddings of 80 and 150 channels: the tiled patch kernel's full
+    # 64-channel chunks plus a partial one, and a ragged last row block
+    ("bf16_step_patch80", synth.CONFIGS["c4"].with_(n_blocks=1, batch=1, tokens=100, hidden=256, heads=2, head_dim=128,
+                                                    mlp_hidden=512, patch_in=80, patch_out=80)),
+    ("bf16_step_patch150_b2", synth.CONFIGS["c4"].with_(n_blocks=1, batch=2, tokens=45, hidden=512, heads=4,
+                                                        head_dim=128, mlp_hidden=512, patch_in=150, patch_out=16)),
+    ("fp32_step_patch33", synth.CONFIGS["c0"].with_(n_blocks=1, batch=1, tokens=40, grid=(5, 8), patch_in=33,
+                                                    patch_out=8)),
     ("bf16_step_class_l3", synth.CONFIGS["c1"].with_(n_blocks=3, batch=2, tokens=64, hidden=256, heads=2,
                                                      head_dim=128, mlp_hidden=512, grid=(8, 8))),
     ("bf16_step_joint_l2", synth.CONFIGS["c3"].with_(n_blocks=2, batch=1, tokens=96, text_tokens=7, hidden=256,
@@ -189,6 +197,13 @@ def test_step_small(name, cfg):
 
 
 # ------------------------------------------------------------------ full-size shapes
+def test_block_max_hidden():
+    """The largest hidden size the library accepts (4096 = 32 heads x 128),
+    MLP 16384, a ragged 70 tokens x 2."""
+    block_case(synth.CONFIGS["c1"].with_(batch=2, tokens=70, hidden=4096, heads=32, head_dim=128, mlp_hidden=16384,
+                                         n_blocks=1))
+
+
 def test_block_c1_full():
     block_case(synth.CONFIGS["c1"].with_(n_blocks=1))
 
