@@ -343,9 +343,21 @@ __global__ __launch_bounds__(NW * 64, WPC) void attn_bf16_pipe_kernel(AttnArgs a
   // Work item (query block, head, sample), query block fastest, taken in
   // contiguous ranges per XCD: the workgroups an XCD runs at once are query
   // blocks of the same head and share its K and V tiles in that XCD's L2.
+  // Units of a split item (the last, partial round) come after the whole
+  // items; consecutive units are the same key range of consecutive items.
   const int Tj = a.Tj, Tjp = a.Tj_pad;
   const int nqb = (Tj + NW * 32 - 1) / (NW * 32);
-  const int item = xcd_remap(blockIdx.x, nqb * a.H * a.B);
+  const int nkv = (Tj + C::BKV - 1) / C::BKV;
+  int item, t0 = 0, t1 = nkv, unit = -1;
+  if ((int)blockIdx.x < a.n_full) {
+    item = xcd_remap(blockIdx.x, a.n_full);
+  } else {
+    unit = xcd_remap(blockIdx.x - a.n_full, a.n_tail * a.split);
+    const int part = unit / a.n_tail;
+    item = a.n_full + (unit - part * a.n_tail);
+    t0 = nkv * part / a.split;
+    t1 = nkv * (part + 1) / a.split;
+  }
   const int qb = item % nqb, bh_i = item / nqb;
   const int h = bh_i % a.H, b = bh_i / a.H;
   const long bh = bh_i;
@@ -354,7 +366,6 @@ __global__ __launch_bounds__(NW * 64, WPC) void attn_bf16_pipe_kernel(AttnArgs a
   const bf16_t* __restrict__ vp = (const bf16_t*)a.v + bh * DH * (long)Tjp;
   const unsigned lds0 = __builtin_amdgcn_readfirstlane(lds_address(smem));
   const int q0 = qb * (NW * 32) + wave * 32;  // first query of this wave
-  const int nkv = (Tj + C::BKV - 1) / C::BKV;
 
   // DMA of one tile (layout as in the kernel above) into slot tile % ST.  The
   // sources are a scalar base (the tile's first K row / V^T column) plus a
@@ -387,13 +398,13 @@ __global__ __launch_bounds__(NW * 64, WPC) void attn_bf16_pipe_kernel(AttnArgs a
   // count, and the vmcnt waits are constants.
   auto issue_one = [&](int tile, int t) {
     const int qi = wave + NW * t;  // wave-uniform
-    const int tl = min(tile, nkv - 1), kv0 = tl * C::BKV;
+    const int tl = min(tile, t1 - 1), kv0 = tl * C::BKV;
     const bf16_t* kb = kp + (long)kv0 * C::DHP;  // wave-uniform
     const bf16_t* vb = vp + kv0;
     const bool kpart = qi < C::KDMA || qi >= C::TDMA;
     const unsigned off = tl == nkv - 1 ? doff_last[t] : doff[t];
-    const unsigned dst = tile < nkv && qi < C::TDMA ? lds0 + (unsigned)((tile % ST) * C::SLOT + qi * 1024)
-                                                     : lds0 + (unsigned)(ST * C::SLOT);
+    const unsigned dst = tile < t1 && qi < C::TDMA ? lds0 + (unsigned)((tile % ST) * C::SLOT + qi * 1024)
+                                                    : lds0 + (unsigned)(ST * C::SLOT);
     dma_16s(kpart ? (const void*)kb : (const void*)vb, off, dst);
   };
   auto issue = [&](int tile) {
@@ -488,18 +499,20 @@ __global__ __launch_bounds__(NW * 64, WPC) void attn_bf16_pipe_kernel(AttnArgs a
   // prologue: tiles 0 .. ST-2 in flight (tile ST-1 is issued in the first
   // iteration); tiles 0 and 1 landed before the loop
 #pragma unroll
-  for (int t = 0; t < ST - 1; ++t) issue(t);
+  for (int t = 0; t < ST - 1; ++t) issue(t0 + t);
   wait_vmcnt<(ST - 3) * IPW>();
   __syncthreads();
-  if (nkv <= 2) {  // the last tile has landed already (else: zeroed at the end of iteration nkv-3)
+  // the sequence's last tile, where this unit's range holds it, has landed
+  // already (else: zeroed at the end of iteration nkv-3)
+  if (t1 == nkv && nkv - 1 <= t0 + 1) {
     zero_v_tail(nkv - 1);
     __syncthreads();
   }
   f32x16 scur[2], snext[2];
-  qk(0, scur);
+  qk(t0, scur);
   float mcur = rowmax(scur);
 
-  for (int j = 0; j < nkv; ++j) {
+  for (int j = t0; j < t1; ++j) {
     // Keys past the end (last tile only) are masked just before their
     // exponentials.  Their K rows repeat row Tj-1, so the unmasked row max
     // taken earlier is still the max over real keys.
@@ -534,7 +547,7 @@ __global__ __launch_bounds__(NW * 64, WPC) void attn_bf16_pipe_kernel(AttnArgs a
     // workgroup's DMA instructions queue at the address unit and stall the
     // waves at issue.
     {
-      const int tn = min(j + 1, nkv - 1), kvn = tn * C::BKV;
+      const int tn = min(j + 1, t1 - 1), kvn = tn * C::BKV;
       const unsigned char* sln = smem + (tn % ST) * C::SLOT;
       constexpr int NQ = 2 * C::KS;  // QK^T MFMAs per tile; MFMA i: half i % 2, k-step i / 2
       auto kread = [&](int i) { return *(const bf16x8*)(sln + (i & 1) * 32 * C::KROW + k_off[i >> 1]); };
@@ -609,7 +622,7 @@ __global__ __launch_bounds__(NW * 64, WPC) void attn_bf16_pipe_kernel(AttnArgs a
     // be done with slot j % ST before it takes tile j+ST
     wait_vmcnt<(ST - 3) * IPW>();
     __syncthreads();
-    if (j + 2 == nkv - 1) {  // the last tile's V^T is read in iteration nkv-1
+    if (t1 == nkv && j + 2 == nkv - 1) {  // the last tile's V^T is read in iteration nkv-1
       zero_v_tail(nkv - 1);
       __syncthreads();
     }
@@ -621,7 +634,26 @@ __global__ __launch_bounds__(NW * 64, WPC) void attn_bf16_pipe_kernel(AttnArgs a
     // with FOLD, l is O^T row DH: element LE of tile LT in the lanes of half
     // LG (the other half holds a zero row there)
     const float l_lane = FOLD ? (g == C::LG ? oacc[C::LT][C::LE] : 0.f) : l_run;
-    const float inv = 1.0f / sum_halves(l_lane);
+    const float l_tot = sum_halves(l_lane);
+    if (unit >= 0) {
+      // a unit of a split item: O relative to its own m_run, m_run and l,
+      // for attn_merge
+      if (qrow < Tj) {
+        float* pr = a.part + ((long)unit * (NW * 32) + wave * 32 + r32) * (DH + 4);
+#pragma unroll
+        for (int t = 0; t < C::DT; ++t)
+#pragma unroll
+          for (int jj = 0; jj < 4; ++jj) {
+            const int d = t * 32 + jj * 8 + g * 4;
+            if (d < DH)
+              *(f32x4*)(pr + d) = f32x4{oacc[t][jj * 4 + 0], oacc[t][jj * 4 + 1], oacc[t][jj * 4 + 2],
+                                        oacc[t][jj * 4 + 3]};
+          }
+        if (g == 0) *(f32x2*)(pr + DH) = f32x2{m_run, l_tot};
+      }
+      return;
+    }
+    const float inv = 1.0f / l_tot;
     if (qrow < Tj) {
       const long orow = qrow < a.T_img ? (long)b * a.T_img + qrow
                                        : (long)a.B * a.T_img + (long)b * a.T_txt + (qrow - a.T_img);
@@ -639,6 +671,77 @@ __global__ __launch_bounds__(NW * 64, WPC) void attn_bf16_pipe_kernel(AttnArgs a
   }
 }
 
+// Merge of the units of the split items: per query, with m = max_s m_s and
+// f_s = 2^(m_s - m),  O = sum_s f_s O_s / sum_s f_s l_s  (ranges in order
+// s = 0, 1, ...), stored as the o row of the query in bf16.  One lane per
+// four columns of one query row.
+template <int DH, int QB>
+__global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
+  constexpr int G = DH / 4;  // column groups per row
+  const long e = blockIdx.x * 256L + threadIdx.x;
+  if (e >= (long)a.n_tail * QB * G) return;
+  const int c4 = (int)(e % G) * 4;
+  const int qr = (int)((e / G) % QB), ti = (int)(e / ((long)G * QB));
+  const int item = a.n_full + ti;
+  const int nqb = (a.Tj + QB - 1) / QB;
+  const int qb = item % nqb, bh = item / nqb, h = bh % a.H, b = bh / a.H;
+  const int qrow = qb * QB + qr;
+  if (qrow >= a.Tj) return;
+  const long stride = (long)a.n_tail * QB * (DH + 4);
+  const float* p0 = a.part + ((long)ti * QB + qr) * (DH + 4);
+  float m = -INFINITY;
+  for (int s = 0; s < a.split; ++s) m = fmaxf(m, p0[s * stride + DH]);
+  float den = 0.f;
+  f32x4 num = {0.f, 0.f, 0.f, 0.f};
+  for (int s = 0; s < a.split; ++s) {
+    const float* ps = p0 + s * stride;
+    const float f = __builtin_amdgcn_exp2f(ps[DH] - m);
+    den += f * ps[DH + 1];
+    const f32x4 o = *(const f32x4*)(ps + c4);
+    num[0] += f * o[0];
+    num[1] += f * o[1];
+    num[2] += f * o[2];
+    num[3] += f * o[3];
+  }
+  const float inv = 1.0f / den;
+  const long orow = qrow < a.T_img ? (long)b * a.T_img + qrow
+                                   : (long)a.B * a.T_img + (long)b * a.T_txt + (qrow - a.T_img);
+  bf16_t* op = (bf16_t*)a.o + orow * a.D + h * DH + c4;
+  *(u32x2*)op = u32x2{pack_bf16x2(num[0] * inv, num[1] * inv), pack_bf16x2(num[2] * inv, num[3] * inv)};
+}
+
+// Items of the pipelined kernel (256 queries each) that fill whole rounds of
+// 256 run whole; the items of the last, partial round are split into S key
+// ranges when that shortens the launch: the last round then takes
+// ceil(n_tail S / 256) / S of a round instead of one, plus ~1% of a round
+// per range for the partial stores and the merge.  Each range keeps at
+// least 4 key tiles.  Video DiT, 17550 tokens: 1656 items = 6 rounds + 120,
+// S = 2; joint DiT, 4352 tokens: 408 = 1 round + 152, S = 5.
+static constexpr int ATTN_PIPE_QUERIES = 256;
+
+size_t attn_split_plan(int B, int H, int Tj, int head_dim, size_t part_cap, int* n_full, int* n_tail, int* split) {
+  const long items = (long)((Tj + ATTN_PIPE_QUERIES - 1) / ATTN_PIPE_QUERIES) * H * B;
+  const int nkv = (Tj + 63) / 64;
+  *n_full = (int)items;
+  *n_tail = 0;
+  *split = 1;
+  const long tail = items % 256;
+  if (items < 256 || tail == 0) return 0;
+  double best = 1.0;
+  int best_s = 1;
+  for (int S = 2; S <= 8 && nkv / S >= 4; ++S) {
+    const size_t bytes = (size_t)S * tail * ATTN_PIPE_QUERIES * (head_dim + 4) * sizeof(float);
+    if (bytes > part_cap) break;
+    const double cost = (double)((tail * S + 255) / 256) / S + 0.01 * S;
+    if (cost < best - 0.05) best = cost, best_s = S;
+  }
+  if (best_s == 1) return 0;
+  *n_full = (int)(items - tail);
+  *n_tail = (int)tail;
+  *split = best_s;
+  return (size_t)best_s * tail * ATTN_PIPE_QUERIES * (head_dim + 4) * sizeof(float);
+}
+
 hipError_t launch_attn_bf16(const AttnArgs& a, int head_dim, hipStream_t st) {
   // Enough work items for every CU, or at least half of them with long
   // sequences (32 key tiles or more, where the steady state dominates, e.g.
@@ -650,10 +753,24 @@ hipError_t launch_attn_bf16(const AttnArgs& a, int head_dim, hipStream_t st) {
   const bool wide = items >= 256 || (items >= 128 && a.Tj >= 2048);
   const int nw = wide ? 8 : 4;
   dim3 grid((a.Tj + nw * 32 - 1) / (nw * 32), a.H, a.B), block(nw * 64);
-  dim3 grid1(grid.x * grid.y * grid.z);  // the pipelined kernel maps a 1-D grid to its items
-#define ATTN_LAUNCH(DHV)                                                                   \
-  if (wide) hipLaunchKernelGGL((attn_bf16_pipe_kernel<DHV, 8>), grid1, block, 0, st, a);  \
-  else hipLaunchKernelGGL((attn_bf16_dma_kernel<DHV, 4, 1>), grid, block, 0, st, a);
+  // the pipelined kernel maps a 1-D grid to its items and split units
+  AttnArgs p = a;
+  if (!wide || !a.part || a.split < 2) {
+    p.n_full = (int)(grid.x * grid.y * grid.z);
+    p.n_tail = 0;
+    p.split = 1;
+  }
+  dim3 grid1(p.n_full + p.n_tail * p.split);
+  const long merge_lanes = (long)p.n_tail * ATTN_PIPE_QUERIES * (head_dim / 4);
+  dim3 grid_m((unsigned)((merge_lanes + 255) / 256));
+#define ATTN_LAUNCH(DHV)                                                                          \
+  if (wide) {                                                                                     \
+    hipLaunchKernelGGL((attn_bf16_pipe_kernel<DHV, 8>), grid1, block, 0, st, p);                   \
+    if (p.n_tail > 0)                                                                             \
+      hipLaunchKernelGGL((attn_merge_kernel<DHV, ATTN_PIPE_QUERIES>), grid_m, dim3(256), 0, st, p); \
+  } else {                                                                                        \
+    hipLaunchKernelGGL((attn_bf16_dma_kernel<DHV, 4, 1>), grid, block, 0, st, a);                  \
+  }
   switch (head_dim) {
     case 64: ATTN_LAUNCH(64) break;
     case 72: ATTN_LAUNCH(72) break;

@@ -11,6 +11,7 @@ typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x2v __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
 // Native 16-byte vector for global/LDS staging (HIP's uint4 is a struct whose
 // copies go through memcpy and can keep staging arrays in scratch memory).
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));

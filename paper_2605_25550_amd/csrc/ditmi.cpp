@@ -549,6 +549,12 @@ dit_status run_block(const dit_shape* s, const Layout& L, char* ws, StreamIO* io
     a.scale = 1.0f / sqrtf((float)dh);
     // the bf16 QKV epilogue stores k already in the exp2 domain
     a.scale_log2 = dt == DIT_BF16 ? 1.0f : (float)(1.4426950408889634 / sqrt((double)dh));
+    // key-range split of the last partial round; its partial results use the
+    // MLP hidden region g, which is dead until fc1
+    if (dt == DIT_BF16) {
+      const size_t g_bytes = (size_t)B * L.Tj * F * E;
+      if (attn_split_plan(B, H, L.Tj, dh, g_bytes, &a.n_full, &a.n_tail, &a.split) > 0) a.part = (float*)gbuf;
+    }
     const double flops = 4.0 * B * H * (double)L.Tj * L.Tj * dh;
     const double bytes = 4.0 * B * (double)L.Tj * D * E;
     HIP_TRY(timed(DIT_K_ATTENTION, flops, bytes, st, [&]() {

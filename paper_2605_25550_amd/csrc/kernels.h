@@ -75,7 +75,20 @@ struct AttnArgs {
   int B, H, Tj, Tj_pad, T_img, T_txt, D;
   float scale_log2;  // factor from q.k to the exp2 domain: log2(e) / sqrt(dh), or 1 where k is stored pre-scaled (bf16)
   float scale;       // 1 / sqrt(dh)
+  // bf16 pipelined kernel, last partial round (attn_split_plan): the first
+  // n_full (query block, head, sample) items run over all keys; each of the
+  // n_tail items after them runs as `split` units over consecutive ranges of
+  // key tiles, which store unnormalised partial results to `part`, and a
+  // merge pass combines them.  split = 1: every item runs whole.
+  int n_full, n_tail, split;
+  float* part;  // [split][n_tail][256 queries][dh + 4] fp32: O (relative to the unit's m), m, l
 };
+
+// Plan of the pipelined attention's last round for B samples, H heads, Tj
+// tokens: n_full items whole, n_tail items split into `split` key ranges.
+// Returns the bytes of partial results it needs (0 without a split); a plan
+// whose partials would exceed part_cap bytes is not used.
+size_t attn_split_plan(int B, int H, int Tj, int head_dim, size_t part_cap, int* n_full, int* n_tail, int* split);
 
 // ------------------------------------------------------------------ LayerNorm + modulate
 struct LnSeg {

@@ -250,6 +250,30 @@ def test_block_row_tail_split():
     assert np.array_equal(y1, y2)
 
 
+ATTN_SPLIT = [
+    # 33 query blocks x 8 heads = 264 items: 256 run whole, the last 8 run as
+    # 8 key ranges each, merged afterwards
+    ("attn_split_dh128", synth.CONFIGS["c4"].with_(tokens=8448, hidden=1024, heads=8, head_dim=128,
+                                                   mlp_hidden=1024, n_blocks=1)),
+    # head_dim 72 (softmax bookkeeping in the MFMA padding): 17 x 16 = 272
+    # items, a ragged last query block
+    ("attn_split_dh72", synth.CONFIGS["c1"].with_(batch=1, tokens=4300, n_blocks=1)),
+]
+
+
+@pytest.mark.parametrize("name,cfg", ATTN_SPLIT, ids=[c[0] for c in ATTN_SPLIT])
+def test_block_attention_split_tail(name, cfg):
+    """The pipelined attention's last, partial round split into key ranges
+    whose partial results are merged: compared in full, and bitwise between
+    two runs (the ranges are merged in a fixed order)."""
+    print(f"[case] attention split tail {name}", flush=True)
+    block_case(cfg)
+    g = _gpu()
+    inp = synth.inputs(cfg)
+    (y1, _), (y2, _) = g.run_block(cfg, synth.block_weights(cfg, 0), inp["x"], inp["cond"], repeat=2)
+    assert np.array_equal(y1, y2)
+
+
 def test_block_joint_split_text_fc1_deterministic():
     """The split ranges are added in a fixed order: two runs agree bitwise."""
     g = _gpu()
