@@ -508,11 +508,14 @@ __global__ __launch_bounds__(NW * 64, WPC) void attn_bf16_pipe_kernel(AttnArgs a
     zero_v_tail(nkv - 1);
     __syncthreads();
   }
-  f32x16 scur[2], snext[2];
-  qk(t0, scur);
-  float mcur = rowmax(scur);
+  f32x16 sa[2], sb[2];
+  qk(t0, sa);
+  float mcur = rowmax(sa);
 
-  for (int j = t0; j < t1; ++j) {
+  // One key tile: the exponentials of scur (tile j) and the QK^T of tile
+  // j+1 into snext.  The loop runs it twice per trip with the roles of the
+  // two score blocks exchanged, so no score block is ever copied.
+  auto tile_step = [&](const int j, f32x16 (&scur)[2], f32x16 (&snext)[2]) __attribute__((always_inline)) {
     // Keys past the end (last tile only) are masked just before their
     // exponentials.  Their K rows repeat row Tj-1, so the unmasked row max
     // taken earlier is still the max over real keys.
@@ -546,6 +549,16 @@ __global__ __launch_bounds__(NW * 64, WPC) void attn_bf16_pipe_kernel(AttnArgs a
     // over the same sequence: issued as a burst after the barrier, the
     // workgroup's DMA instructions queue at the address unit and stall the
     // waves at issue.
+    u32x4 pw[4];
+    // V^T fragments of tile j (landed long before): the first two are read
+    // during the last QK^T MFMAs, so the PV product starts without waiting.
+    const unsigned char* slv = smem + (j % ST) * C::SLOT;
+    constexpr int NP = 4 * C::DT;  // PV MFMAs per tile; MFMA i: key chunk i / DT, O^T tile i % DT
+    auto vread = [&](int i) {
+      const int c = i / C::DT, t = i % C::DT;
+      return *(const u32x4*)(slv + t * 32 * 128 + v_off[c]);
+    };
+    u32x4 vf[3];
     {
       const int tn = min(j + 1, t1 - 1), kvn = tn * C::BKV;
       const unsigned char* sln = smem + (tn % ST) * C::SLOT;
@@ -559,36 +572,27 @@ __global__ __launch_bounds__(NW * 64, WPC) void attn_bf16_pipe_kernel(AttnArgs a
         if (i + 2 < NQ) kf[(i + 2) % 3] = kread(i + 2);
         snext[i & 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[i % 3], qf[i >> 1], i < 2 ? sinit : snext[i & 1],
                                                                0, 0, 0);
+        if (i == NQ - 2) vf[0] = vread(0);
+        if (i == NQ - 1) vf[1] = vread(1);
 #pragma unroll
         for (int t = 0; t < IPW; ++t)
           if (i == 1 + t * (NQ - 1) / IPW) issue_one(j + ST - 1, t);
 #pragma unroll
         for (int e = i * 32 / NQ; e < (i + 1) * 32 / NQ; ++e)
           scur[e >> 4][e & 15] = __builtin_amdgcn_exp2f(scur[e >> 4][e & 15]);
+        // each pair of probabilities is packed to bf16 as soon as both exist:
+        // scores 2p and 2p+1 of the lane's 32 (half p / 8) form word p % 4 of
+        // the B operand of the PV MFMAs over key chunk p / 4
+#pragma unroll
+        for (int p = 0; p < 16; ++p)
+          if (2 * p + 1 >= i * 32 / NQ && 2 * p + 1 < (i + 1) * 32 / NQ)
+            pw[p >> 2][p & 3] = pack_bf16x2(scur[p >> 3][(2 * p) & 15], scur[p >> 3][(2 * p + 1) & 15]);
         __builtin_amdgcn_sched_barrier(0);
       }
-    }
-    u32x4 pw[4];
-#pragma unroll
-    for (int c = 0; c < 4; ++c) {
-      const int kt = c >> 1, jb = (c & 1) * 2;
-      pw[c] = u32x4{pack_bf16x2(scur[kt][jb * 4 + 0], scur[kt][jb * 4 + 1]),
-                    pack_bf16x2(scur[kt][jb * 4 + 2], scur[kt][jb * 4 + 3]),
-                    pack_bf16x2(scur[kt][jb * 4 + 4], scur[kt][jb * 4 + 5]),
-                    pack_bf16x2(scur[kt][jb * 4 + 6], scur[kt][jb * 4 + 7])};
     }
     // PV of tile j (consecutive MFMAs on different O^T tiles), V^T read two
     // MFMAs ahead, interleaved with the row max of tile j+1.
     {
-      const unsigned char* sl = smem + (j % ST) * C::SLOT;
-      constexpr int NP = 4 * C::DT;  // MFMA i: key chunk i / DT, O^T tile i % DT
-      auto vread = [&](int i) {
-        const int c = i / C::DT, t = i % C::DT;
-        return *(const u32x4*)(sl + t * 32 * 128 + v_off[c]);
-      };
-      u32x4 vf[3];
-      vf[0] = vread(0);
-      vf[1] = vread(1);
       float m = -INFINITY, lsum = 0.f;
 #pragma unroll
       for (int i = 0; i < NP; ++i) {
@@ -615,8 +619,6 @@ __global__ __launch_bounds__(NW * 64, WPC) void attn_bf16_pipe_kernel(AttnArgs a
       mcur = max_halves(m);
       if (!FOLD) l_run += lsum;
     }
-#pragma unroll
-    for (int kt = 0; kt < 2; ++kt) scur[kt] = snext[kt];
     // tile j+2 must have landed for every wave before the next iteration's
     // QK^T (tiles j+3 .. j+ST-1 may still be in flight), and every wave must
     // be done with slot j % ST before it takes tile j+ST
@@ -626,7 +628,13 @@ __global__ __launch_bounds__(NW * 64, WPC) void attn_bf16_pipe_kernel(AttnArgs a
       zero_v_tail(nkv - 1);
       __syncthreads();
     }
+  };
+  int j = t0;
+  for (; j + 1 < t1; j += 2) {
+    tile_step(j, sa, sb);
+    tile_step(j + 1, sb, sa);
   }
+  if (j < t1) tile_step(j, sa, sb);
   wait_vmcnt<0>();
 
   {
