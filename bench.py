@@ -221,8 +221,11 @@ def summarize_profile(key, trace_dir, pmc_dir, fetch_dir, write_dir, bench_json,
             row[c] = per_dispatch(pmc, c)
         dur = mean_dur_ns(pmc)
         row["pmc_dispatch_us"] = dur / 1e3 if dur else None
-        # GRBM_GUI_ACTIVE is summed over the 8 XCDs
-        row["clock_ghz"] = row["GRBM_GUI_ACTIVE"] / 8 / dur if dur and row["GRBM_GUI_ACTIVE"] else None
+        # GRBM_GUI_ACTIVE is summed over the 8 XCDs.  It also counts the
+        # counter pass's own per-dispatch overhead, so it gives the clock
+        # only for dispatches long against that (>= 100 us).
+        long_enough = dur is not None and dur >= 100e3
+        row["clock_ghz"] = row["GRBM_GUI_ACTIVE"] / 8 / dur if long_enough and row["GRBM_GUI_ACTIVE"] else None
         fb, wb = per_dispatch(fetch, "FETCH_SIZE"), per_dispatch(write, "WRITE_SIZE")
         row["fetch_bytes"] = fb * 1024 / f_fac if fb is not None else None
         row["write_bytes"] = wb * 1024 / w_fac if wb is not None else None
@@ -259,7 +262,9 @@ def summarize_profile(key, trace_dir, pmc_dir, fetch_dir, write_dir, bench_json,
          "Columns: trace average per launch; algorithmic TFLOP/s and % of the 2.5 PFLOP/s dense bf16 peak; "
          "MfmaUtil = MFMA-busy cycles / (GRBM active cycles x SIMDs); MFMA ops / algorithmic flops "
          "(MOPS x 512; above 1 where MFMA tiles are padded, e.g. head_dim 72 -> 80); clock = GRBM active "
-         "cycles per XCD / dispatch time in the counter pass; LDS = LdsUtil and LDSBankConflict (% of "
+         "cycles per XCD / dispatch time in the counter pass, shown for dispatches of at least 100 us only (the "
+         "GRBM count includes the counter pass's per-dispatch overhead, which also makes MfmaUtil understate "
+         "short dispatches); LDS = LdsUtil and LDSBankConflict (% of "
          "active cycles); VALU = VALUBusy; HBM = FETCH_SIZE and WRITE_SIZE per launch, each divided by "
          f"what the counter reads for a {copy_mib} MiB device copy (fetch factor {f_fac:.3f}, write factor "
          f"{w_fac:.3f}), against the algorithmic bytes of the launch.", "",
