@@ -239,7 +239,9 @@ __global__ __launch_bounds__(NW * 64, QT == 1 ? 8 / NW : 1) void attn_bf16_dma_k
         if (first || __builtin_amdgcn_ballot_w64(mloc > TAU) != 0) {
           const float m_new = bf2f(f2bf(m_run[qt] + (first ? mloc : fmaxf(mloc, 0.f))));
           const float delta = m_new - m_run[qt];
-          const float alpha = __builtin_amdgcn_exp2f(-delta);
+          // O and l are still zero at the first tile, whose max may lie far
+          // below 0 (exp2(-delta) = inf there, and 0 * inf is NaN)
+          const float alpha = first ? 1.0f : __builtin_amdgcn_exp2f(-delta);
 #pragma unroll
           for (int t = 0; t < C::DT; ++t) oacc[qt][t] *= alpha;
 #pragma unroll
@@ -527,7 +529,9 @@ __global__ __launch_bounds__(NW * 64, WPC) void attn_bf16_pipe_kernel(AttnArgs a
       float m_new = m_run + (first ? mcur : fmaxf(mcur, 0.f));
       if (FOLD) m_new = bf2f(f2bf(m_new));  // enters the product as a bf16 operand
       const float delta = m_new - m_run;     // exact
-      const float alpha = __builtin_amdgcn_exp2f(-delta);
+      // O and l are still zero at the first tile, whose max may lie far below
+      // 0 (exp2(-delta) = inf there, and 0 * inf is NaN)
+      const float alpha = first ? 1.0f : __builtin_amdgcn_exp2f(-delta);
       if (!FOLD) l_run *= alpha;
 #pragma unroll
       for (int t = 0; t < C::DT; ++t) oacc[t] *= alpha;
