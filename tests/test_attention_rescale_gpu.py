@@ -126,3 +126,25 @@ def test_first_tile_far_below_zero(name, scale, amp, boundary):
           f"below -128", flush=True)
     assert n_low >= 8, (name, boundary, n_low)
     _compare(f"{name}/low{boundary}", cfg, w, x, c)
+
+
+def test_split_key_ranges_lazy_max():
+    """The pipelined kernel's last, partial round of work items runs as key
+    ranges merged afterwards (33 query blocks x 8 heads = 264 items: the last
+    8, queries 6400.. of head 7, as 8 ranges of 16-17 key tiles).  Tokens
+    before 1280 point against those after it, so for every split query the
+    first tile of ranges 0 and 1 lies below -128 and, inside range 1, tile 20
+    leads tiles 16-19 by more than 64 (log2 units)."""
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    cfg = synth.CONFIGS["c4"].with_(tokens=8448, hidden=1024, heads=8, head_dim=128, mlp_hidden=1024, n_blocks=1)
+    w, x, c = _case(cfg, 1280, 8.0, amp=6.0, sign=-1)
+    s = _scores(cfg, w, x, c)[0, 7, 6400:]
+    low0 = int((s[:, :64].max(-1) < -128.0).sum())
+    low1 = int((s[:, 16 * 64:17 * 64].max(-1) < -128.0).sum())
+    lead = s[:, 20 * 64:21 * 64].max(-1) - s[:, 16 * 64:20 * 64].max(-1)
+    frac = float((lead > 64.0).mean())
+    print(f"[rescale] split ranges: {low0} / {low1} split queries with range 0 / 1 starting below -128, "
+          f"{frac:.2f} moving the max inside range 1", flush=True)
+    assert low0 >= 1000 and low1 >= 1000 and frac > 0.8, (low0, low1, frac)
+    _compare("split_ranges", cfg, w, x, c)
