@@ -566,6 +566,7 @@ __global__ __launch_bounds__(NW * 64, WPC) void attn_bf16_pipe_kernel(AttnArgs a
     // attention -2.7%, joint -2%, DiT-XL/2 at 1024 tokens -1.5%).
     constexpr int EX = 16;
     constexpr int NPRE = EX / 8 * C::DT;  // PV MFMAs before the first one on chunk EX / 8
+    constexpr int ND = 3;  // PV MFMAs issued after the barrier
     auto vread = [&](int i) {
       const int c = i / C::DT, t = i % C::DT;
       return *(const u32x4*)(slv + t * 32 * 128 + v_off[c]);
@@ -609,9 +610,10 @@ __global__ __launch_bounds__(NW * 64, WPC) void attn_bf16_pipe_kernel(AttnArgs a
 #pragma unroll
       for (int i = 0; i < NP; ++i) {
         if (i + 2 < NP) vf[(i + 2) % 3] = vread(i + 2);
-        oacc[i % C::DT] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, vf[i % 3]),
-                                                                  __builtin_bit_cast(bf16x8, pw[i / C::DT]),
-                                                                  oacc[i % C::DT], 0, 0, 0);
+        if (i < NP - ND)
+          oacc[i % C::DT] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, vf[i % 3]),
+                                                                    __builtin_bit_cast(bf16x8, pw[i / C::DT]),
+                                                                    oacc[i % C::DT], 0, 0, 0);
 #pragma unroll
         for (int e = i * 32 / NP; e < (i + 1) * 32 / NP; ++e) m = fmaxf(m, snext[e >> 4][e & 15]);
         // exponentials and packing of chunks EX / 8 .. 3
@@ -646,6 +648,16 @@ __global__ __launch_bounds__(NW * 64, WPC) void attn_bf16_pipe_kernel(AttnArgs a
     // be done with slot j % ST before it takes tile j+ST
     wait_vmcnt<(ST - 3) * IPW>();
     __syncthreads();
+    // the last ND PV MFMAs of the tile, on fragments already in registers
+    // (the barrier's fence has waited for their LDS reads): the matrix pipe
+    // has work while the next tile's first K fragments load (measured: video
+    // DiT attention -2.5%, joint -1.5%, DiT-XL/2 at 1024 tokens -2%; deferring
+    // four or six instead is no faster)
+#pragma unroll
+    for (int i = NP - ND; i < NP; ++i)
+      oacc[i % C::DT] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, vf[i % 3]),
+                                                                __builtin_bit_cast(bf16x8, pw[i / C::DT]),
+                                                                oacc[i % C::DT], 0, 0, 0);
     if (t1 == nkv && j + 2 == nkv - 1) {  // the last tile's V^T is read in iteration nkv-1
       zero_v_tail(nkv - 1);
       __syncthreads();
