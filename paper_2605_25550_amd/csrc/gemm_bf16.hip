@@ -84,14 +84,39 @@ struct Epilogue {
   static constexpr int gcd(int a, int b) { return b == 0 ? a : gcd(b, a % b); }
   static constexpr int NCG = CPR / gcd(64, CPR);
   static_assert(32 * WTN % 256 == 0, "slab must split evenly over 64 lanes");
+  static constexpr bool QKV = EPI == EPI_QKV;
   f32x4 bias4[NCG];           // bias of the lane's column groups (row path)
-  float vb[EPI == EPI_QKV ? PL : 1];  // v path: bias of the column of each group
+  float vb[QKV ? PL : 1];     // v path: bias of the column of each group
   f32x4 gate4[RES ? NCG : 1]; // EPI_RESID: gate of sample b0 for the lane's column groups
   int b0;
+  float inv_rpb;              // 1 / rows_per_batch, for div_exact
+  // EPI_QKV, q and k columns: for each column group of the lane, its head's
+  // column block of q or k (element h Tj qk_stride + d), the factor it is
+  // stored with, and whether it is the head's last group, after which the
+  // padding columns are written too (0: no, 1: of q, 2: of k).
+  bf16_t* qk_col[QKV ? NCG : 1];
+  float qk_f[QKV ? NCG : 1];
+  int qk_pad[QKV ? NCG : 1];
 
   __device__ __forceinline__ void init(const GemmProb& P, int nw0, int mfirst, bool vcols, int lane) {
     const bf16_t* __restrict__ bias = (const bf16_t*)P.bias;
     const int N = P.N;
+    // Reciprocals for div_exact, computed once: a division written in the
+    // per-group code is expanded in full for every unrolled copy.
+    inv_rpb = 1.0f / (float)P.rows_per_batch;
+    if (QKV && !vcols) {
+      const int D = P.hidden, dh = P.head_dim;
+      const float inv_dh = 1.0f / (float)dh;
+#pragma unroll
+      for (int q = 0; q < NCG; ++q) {
+        const int n = min(nw0 + ((lane + 64 * q) % CPR) * 4, N - 4);  // clamped: ragged strips
+        const int sel = n >= D ? 1 : 0, rem = n - sel * D;  // q or k (v tiles take the other path)
+        const int h = div_exact(rem, dh, inv_dh), d = rem - h * dh;
+        qk_col[q] = (bf16_t*)(sel == 0 ? P.q : P.k) + (long)h * P.Tj * P.qk_stride + d;
+        qk_f[q] = sel == 0 ? 1.0f : P.k_scale;  // k in the softmax's exp2 domain, rounded once
+        qk_pad[q] = d + 4 == dh && P.qk_stride > dh ? 1 + sel : 0;
+      }
+    }
     if (EPI == EPI_QKV && vcols) {
 #pragma unroll
       for (int it = 0; it < PL; ++it) {
@@ -101,7 +126,7 @@ struct Epilogue {
     }
     if (RES) {
       const int rpb = P.rows_per_batch;
-      b0 = div_exact(min(mfirst, P.M - 1), rpb, 1.0f / (float)rpb);
+      b0 = div_exact(min(mfirst, P.M - 1), rpb, inv_rpb);
     }
 #pragma unroll
     for (int q = 0; q < NCG; ++q) {
@@ -128,11 +153,12 @@ struct Epilogue {
   __device__ __forceinline__ void apply(const GemmProb& P, const float* Cw, int mb, int nw0, bool vcols, int lane,
                                         const f32x4 (&x)[NX]) const {
     const int rpb = P.rows_per_batch, M = P.M, N = P.N;
-    const float inv_rpb = 1.0f / (float)rpb;  // wave-uniform, for div_exact
     if (EPI == EPI_QKV && vcols) {
       // v^T[b][h][d][j]: lane takes one column and four consecutive rows.
-      const int D = P.hidden, dh = P.head_dim;
-      const float inv_dh = 1.0f / (float)dh;
+      // Element ((b H + h) dh + d) Tj_pad + v_key_pos(j), and h dh + d is the
+      // column's offset n - 2D within the v block, so a lane's four rows
+      // (fixed for the slab) give one row base and each column adds n Tj_pad.
+      const int D = P.hidden;
       float cv[PL][4];  // all LDS reads first: one wait for the slab, not one per group
 #pragma unroll
       for (int it = 0; it < PL; ++it) {
@@ -141,24 +167,25 @@ struct Epilogue {
 #pragma unroll
         for (int e = 0; e < 4; ++e) cv[it][e] = Cw[(r4 + e) * CST + col];
       }
+      const int m = mb + (lane & 7) * 4;  // the lane's first row: (c & 7) == (lane & 7)
+      if (m >= M) return;
+      const int b = div_exact(m, rpb, inv_rpb), j = m - b * rpb;
+      const int jp = j + P.seq_off;
+      const bool four = m + 3 < M && j + 3 < rpb && (jp & 3) == 0;  // 4 keys stay contiguous under v_key_pos
+      bf16_t* const vrow = (bf16_t*)P.v + ((long)b * D - 2 * D) * P.Tj_pad + v_key_pos(jp);
 #pragma unroll
       for (int it = 0; it < PL; ++it) {
-        const int c = lane + 64 * it;
-        const int col = c >> 3, r4 = (c & 7) * 4;
-        const int n = nw0 + col, m = mb + r4;
-        if (n >= N || m >= M) continue;
-        const int rem = n - 2 * D, h = div_exact(rem, dh, inv_dh), d = rem - h * dh;
+        const int n = nw0 + ((lane + 64 * it) >> 3);
+        if (n >= N) continue;
         const float bv = vb[it];
-        const int b = div_exact(m, rpb, inv_rpb), jp = m - b * rpb + P.seq_off;
         const float v0 = cv[it][0] + bv, v1 = cv[it][1] + bv, v2 = cv[it][2] + bv, v3 = cv[it][3] + bv;
-        if (m + 3 < M && jp - P.seq_off + 3 < rpb && (jp & 3) == 0) {  // 4 keys stay contiguous under v_key_pos
-          bf16_t* vt = (bf16_t*)P.v + (((long)b * P.heads + h) * dh + d) * P.Tj_pad + v_key_pos(jp);
-          *(u32x2*)vt = u32x2{pack_bf16x2(v0, v1), pack_bf16x2(v2, v3)};
+        if (four) {
+          *(u32x2*)(vrow + (long)n * P.Tj_pad) = u32x2{pack_bf16x2(v0, v1), pack_bf16x2(v2, v3)};
         } else {
           const float vv[4] = {v0, v1, v2, v3};
           for (int e = 0; e < 4 && m + e < M; ++e) {
             const int be = div_exact(m + e, rpb, inv_rpb), je = (m + e) - be * rpb + P.seq_off;
-            ((bf16_t*)P.v)[(((long)be * P.heads + h) * dh + d) * P.Tj_pad + v_key_pos(je)] = f2bf(vv[e]);
+            ((bf16_t*)P.v)[((long)be * D + n - 2 * D) * P.Tj_pad + v_key_pos(je)] = f2bf(vv[e]);
           }
         }
       }
@@ -199,19 +226,16 @@ struct Epilogue {
       } else if (EPI == EPI_STORE) {
         *(f32x4*)((float*)P.out + (long)m * N + n) = f32x4{y0, y1, y2, y3};
       } else {  // EPI_QKV, q and k columns: 4 consecutive d of one head
-        const int D = P.hidden, dh = P.head_dim;
-        const int s = div_exact(n, D, 1.0f / (float)D), rem = n - s * D;
-        const int h = div_exact(rem, dh, 1.0f / (float)dh), d = rem - h * dh;
         const int b = div_exact(m, rpb, inv_rpb), jp = m - b * rpb + P.seq_off;
-        bf16_t* dst = (bf16_t*)(s == 0 ? P.q : P.k) + (((long)b * P.heads + h) * P.Tj + jp) * P.qk_stride + d;
-        const float f = s == 0 ? 1.0f : P.k_scale;  // k in the softmax's exp2 domain, rounded once
+        bf16_t* dst = qk_col[it % NCG] + ((long)b * P.heads * P.Tj + jp) * P.qk_stride;
+        const float f = qk_f[it % NCG];
         *(u32x2*)dst = u32x2{pack_bf16x2(y0 * f, y1 * f), pack_bf16x2(y2 * f, y3 * f)};
         // The row's padding (head_dim 72 -> 80) is zero, except k's column
         // head_dim, which is 1: there the attention kernel folds the running
         // softmax max into the QK^T product.
-        if (d + 4 == dh && P.qk_stride > dh)
-          for (int z = 4; z < P.qk_stride - dh + 4; z += 4)
-            *(u32x2*)(dst + z) = u32x2{s == 1 && z == 4 ? 0x3F80u : 0u, 0u};
+        if (qk_pad[it % NCG])
+          for (int z = 4; z < P.qk_stride - P.head_dim + 4; z += 4)
+            *(u32x2*)(dst + z) = u32x2{qk_pad[it % NCG] == 2 && z == 4 ? 0x3F80u : 0u, 0u};
       }
     }
   }
