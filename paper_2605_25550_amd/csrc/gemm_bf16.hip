@@ -197,21 +197,18 @@ struct Epilogue {
       const int c = lane + 64 * it;
       cy[it] = *(const f32x4*)&Cw[(c / CPR) * CST + (c % CPR) * 4];
     }
-#pragma unroll
-    for (int it = 0; it < PL; ++it) {
-      const int c = lane + 64 * it;
-      const int row = c / CPR, c4 = (c % CPR) * 4;
-      const int m = mb + row, n = nw0 + c4;
-      if (m >= M || n >= N) continue;  // N is a multiple of 4
+    // Group it of the lane: row m, column n, element m N + n.  b: the row's
+    // sample where it is known (-1: find it).
+    auto group = [&](int it, int m, int n, long off, int b) __attribute__((always_inline)) {
       const f32x4 y = cy[it];
       if ((RES || EPI == EPI_GELU) && P.ksplit > 1) {  // one k-range: raw fp32 partial (P.part at its range)
-        *(f32x4*)(P.part + (long)m * N + n) = y;
-        continue;
+        *(f32x4*)(P.part + off) = y;
+        return;
       }
       const f32x4 bq = bias4[it % NCG];
       const float y0 = y[0] + bq[0], y1 = y[1] + bq[1], y2 = y[2] + bq[2], y3 = y[3] + bq[3];
       if (RES) {
-        const int b = div_exact(m, rpb, inv_rpb);
+        if (b < 0) b = div_exact(m, rpb, inv_rpb);
         f32x4 g = gate4[it % NCG];
         if (b != b0) g = *(const f32x4*)(P.gate + (long)b * P.gate_stride + n);  // strip spans two samples
         f32x4 xv = x[it];
@@ -219,14 +216,15 @@ struct Epilogue {
         xv[1] += g[1] * y1;
         xv[2] += g[2] * y2;
         xv[3] += g[3] * y3;
-        *(f32x4*)(P.resid + (long)m * N + n) = xv;
+        *(f32x4*)(P.resid + off) = xv;
       } else if (EPI == EPI_GELU) {
-        *(u32x2*)((bf16_t*)P.out + (long)m * N + n) =
+        *(u32x2*)((bf16_t*)P.out + off) =
             u32x2{pack_bf16x2(gelu_tanh(y0), gelu_tanh(y1)), pack_bf16x2(gelu_tanh(y2), gelu_tanh(y3))};
       } else if (EPI == EPI_STORE) {
-        *(f32x4*)((float*)P.out + (long)m * N + n) = f32x4{y0, y1, y2, y3};
+        *(f32x4*)((float*)P.out + off) = f32x4{y0, y1, y2, y3};
       } else {  // EPI_QKV, q and k columns: 4 consecutive d of one head
-        const int b = div_exact(m, rpb, inv_rpb), jp = m - b * rpb + P.seq_off;
+        if (b < 0) b = div_exact(m, rpb, inv_rpb);
+        const int jp = m - b * rpb + P.seq_off;
         bf16_t* dst = qk_col[it % NCG] + ((long)b * P.heads * P.Tj + jp) * P.qk_stride;
         const float f = qk_f[it % NCG];
         *(u32x2*)dst = u32x2{pack_bf16x2(y0 * f, y1 * f), pack_bf16x2(y2 * f, y3 * f)};
@@ -237,6 +235,29 @@ struct Epilogue {
           for (int z = 4; z < P.qk_stride - P.head_dim + 4; z += 4)
             *(u32x2*)(dst + z) = u32x2{qk_pad[it % NCG] == 2 && z == 4 ? 0x3F80u : 0u, 0u};
       }
+    };
+    // A slab inside the matrix whose 32 rows belong to one sample (a lane's
+    // column is the same in every group when CPR divides 64): no bounds
+    // checks, one sample, and the row advances by 64 / CPR per group.
+    bool fast = NCG == 1 && mb + 32 <= M && nw0 + WTN <= N;
+    int bs = -1;
+    if (fast && (RES || EPI == EPI_QKV)) {
+      bs = div_exact(mb, rpb, inv_rpb);
+      fast = div_exact(mb + 31, rpb, inv_rpb) == bs;
+    }
+    if (fast) {
+      const int m = mb + lane / CPR, n = nw0 + (lane % CPR) * 4;
+      const long off = (long)m * N + n;
+#pragma unroll
+      for (int it = 0; it < PL; ++it) group(it, m + (64 / CPR) * it, n, off + (long)((64 / CPR) * it) * N, bs);
+      return;
+    }
+#pragma unroll
+    for (int it = 0; it < PL; ++it) {
+      const int c = lane + 64 * it;
+      const int m = mb + c / CPR, n = nw0 + (c % CPR) * 4;
+      if (m >= M || n >= N) continue;  // N is a multiple of 4
+      group(it, m, n, (long)m * N + n, -1);
     }
   }
 };
