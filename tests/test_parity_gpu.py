@@ -92,6 +92,13 @@ SMALL = [
     ("bf16_xl_b4_split", synth.CONFIGS["c1"].with_(batch=4, n_blocks=1)),
     # 2340 rows -> QKV (incl. the v^T columns) and fc1 on 256x256 tiles
     ("bf16_xl_t260_b9_tiles", synth.CONFIGS["c1"].with_(batch=9, tokens=260, n_blocks=1)),
+    # 600 rows (and 512 + 64 joint rows) at widths that are multiples of 144:
+    # the QKV projection takes the 64x144 tiles, whose 48-column wave strips
+    # give each lane three column groups (q/k heads, head_dim 72 padding,
+    # v^T columns, text rows after the image rows)
+    ("bf16_qkv_144_dh72", synth.CONFIGS["c1"].with_(batch=2, tokens=300, n_blocks=1)),
+    ("bf16_joint_qkv_144", synth.CONFIGS["c3"].with_(batch=1, tokens=512, text_tokens=64, hidden=1152, heads=9,
+                                                     head_dim=128, mlp_hidden=1024, n_blocks=1)),
     # >= 256 (sample, head, 256-query) items select the software-pipelined
     # attention kernel: one, two and three key tiles, ragged last tiles
     ("bf16_pipe_dh64_t17_b16", synth.CONFIGS["c1"].with_(batch=16, tokens=17, hidden=1024, heads=16, head_dim=64,
