@@ -73,6 +73,20 @@ def build_probe() -> str:
     return PROBE
 
 
+MFMA_PROBE = os.path.join(PKG, "mfma_probe")
+
+
+def build_mfma_probe() -> str:
+    """The MFMA throughput and clock probe (csrc/mfma_probe.hip, a
+    measurement tool, standalone)."""
+    cmd = [hipcc(), f"--offload-arch={ARCH}", "-O3", "-std=c++17", *DEVICE_FLAGS,
+           os.path.join(CSRC, "mfma_probe.hip"), "-o", MFMA_PROBE]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"mfma probe build failed:\n{r.stdout}{r.stderr}")
+    return MFMA_PROBE
+
+
 # Host-code sanitizers for the CPU tests of the C ABI: the host side
 # (ditmi.cpp: validation, workspace layout, tile planning, launch sequencing)
 # is rebuilt with AddressSanitizer and UndefinedBehaviorSanitizer; the kernel
