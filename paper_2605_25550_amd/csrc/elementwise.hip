@@ -413,8 +413,15 @@ __global__ __launch_bounds__(256) void patch_tile_kernel(int rows, int T, int P,
       zs[r][c] = r < nr && c < pc ? z[(long)(r0 + r) * P + p0 + c] : 0.f;
     }
     float wv[PT_CHUNK];
+    if (col && pc == PT_CHUNK && P % 8 == 0) {
+      // the lane's 64 weights as 16-byte loads (8 elements each, aligned:
+      // n P + p0 + c is a multiple of 8)
 #pragma unroll
-    for (int c = 0; c < PT_CHUNK; ++c) wv[c] = col && c < pc ? ld_as_float<WT>(w, (long)n * P + p0 + c) : 0.f;
+      for (int c = 0; c < PT_CHUNK; c += 8) W8<WT>::load(w + (long)n * P + p0 + c, &wv[c]);
+    } else {
+#pragma unroll
+      for (int c = 0; c < PT_CHUNK; ++c) wv[c] = col && c < pc ? ld_as_float<WT>(w, (long)n * P + p0 + c) : 0.f;
+    }
     __syncthreads();
     if (pc == PT_CHUNK) {
 #pragma unroll
