@@ -548,11 +548,7 @@ __global__ __launch_bounds__(NW * 64, WPC) void attn_bf16_pipe_kernel(AttnArgs a
     // (unconditional: the last iteration recomputes the last tile, unused):
     // K fragments are read two MFMAs ahead, the MFMAs alternate between the
     // two 32-key halves (independent accumulators), and each MFMA is
-    // followed by its share of the exponentials.  The DMA of tile j+ST-1
-    // into the slot of tile j-1 (released by the last barrier) is spread
-    // over the same sequence: issued as a burst after the barrier, the
-    // workgroup's DMA instructions queue at the address unit and stall the
-    // waves at issue.
+    // followed by its share of the exponentials.
     u32x4 pw[4];
     // V^T fragments of tile j (landed long before): the first two are read
     // during the last QK^T MFMAs, so the PV product starts without waiting.
@@ -587,9 +583,7 @@ __global__ __launch_bounds__(NW * 64, WPC) void attn_bf16_pipe_kernel(AttnArgs a
                                                                0, 0, 0);
         if (i == NQ - 2) vf[0] = vread(0);
         if (i == NQ - 1) vf[1] = vread(1);
-#pragma unroll
-        for (int t = 0; t < IPW; ++t)
-          if (i == 1 + t * (NQ - 1) / IPW) issue_one(j + ST - 1, t);
+
 #pragma unroll
         for (int e = i * EX / NQ; e < (i + 1) * EX / NQ; ++e)
           scur[e >> 4][e & 15] = __builtin_amdgcn_exp2f(scur[e >> 4][e & 15]);
@@ -604,12 +598,21 @@ __global__ __launch_bounds__(NW * 64, WPC) void attn_bf16_pipe_kernel(AttnArgs a
       }
     }
     // PV of tile j (consecutive MFMAs on different O^T tiles), V^T read two
-    // MFMAs ahead, interleaved with the row max of tile j+1.
+    // MFMAs ahead, interleaved with the row max of tile j+1.  The DMA of tile
+    // j+ST-1 into the slot of tile j-1 (released by the last barrier) is
+    // spread over the same sequence, one instruction every few MFMAs: issued
+    // as a burst after the barrier, the workgroup's DMA instructions queue at
+    // the address unit and stall the waves at issue.  Placed here rather than
+    // beside the QK^T MFMAs, which carry half the exponentials, it measured
+    // video DiT attention -1%, DiT-XL/2 at 1024 tokens -1.6%.
     {
       float m = -INFINITY, lsum = 0.f;
 #pragma unroll
       for (int i = 0; i < NP; ++i) {
         if (i + 2 < NP) vf[(i + 2) % 3] = vread(i + 2);
+#pragma unroll
+        for (int t = 0; t < IPW; ++t)
+          if (i == t * (NP - ND) / IPW) issue_one(j + ST - 1, t);
         if (i < NP - ND)
           oacc[i % C::DT] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, vf[i % 3]),
                                                                     __builtin_bit_cast(bf16x8, pw[i / C::DT]),
