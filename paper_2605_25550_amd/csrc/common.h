@@ -33,12 +33,6 @@ template <typename T> __device__ __forceinline__ float ld_as_float(const T* p, l
 template <> __device__ __forceinline__ float ld_as_float<float>(const float* p, long i) { return p[i]; }
 template <> __device__ __forceinline__ float ld_as_float<bf16_t>(const bf16_t* p, long i) { return bf2f(p[i]); }
 
-__device__ __forceinline__ float warp_sum(float v) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
-  return v;
-}
-
 // Sum over the 64 lanes: DPP moves combine within each 16-lane row (lane
 // pairs, quads, half-row mirror, row mirror), then the four row sums are read
 // as scalars.  No LDS-crossbar permutes; every lane receives the total.
@@ -66,9 +60,6 @@ __device__ __forceinline__ int div_exact(int n, int d, float inv) {
   q += (q + 1) * d <= n ? 1 : 0;
   return q;
 }
-
-// Value held by lane (l ^ 32): the other half of a 64-wide wavefront.
-__device__ __forceinline__ float other_half(float v) { return __shfl_xor(v, 32, 64); }
 
 // max / sum of v over lanes l and l ^ 32.  v_permlane32_swap exchanges the
 // upper half of its first operand with the lower half of its second; with
