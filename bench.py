@@ -347,9 +347,11 @@ class Workload:
 
 
 def algorithmic_flops(cfg) -> float:
-    """GEMM (24 B T D^2 per stream-block) + attention (4 B Tj^2 D per block)."""
-    T, Tt, B, D = cfg.tokens, cfg.text_tokens, cfg.batch, cfg.hidden
-    return cfg.n_blocks * (24.0 * B * (T + Tt) * D * D + 4.0 * B * (T + Tt) ** 2 * D)
+    """GEMMs (2 B T D (3D + D + 2 F) per stream-block: QKV, output projection,
+    fc1 and fc2 with MLP width F; 24 B T D^2 at F = 4D) + attention
+    (4 B Tj^2 D per block over the joint sequence Tj)."""
+    T, Tt, B, D, F = cfg.tokens, cfg.text_tokens, cfg.batch, cfg.hidden, cfg.mlp_hidden
+    return cfg.n_blocks * (2.0 * B * (T + Tt) * D * (4 * D + 2 * F) + 4.0 * B * (T + Tt) ** 2 * D)
 
 
 def host_info() -> dict:
