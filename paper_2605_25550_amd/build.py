@@ -87,6 +87,20 @@ def build_mfma_probe() -> str:
     return MFMA_PROBE
 
 
+HBM_PROBE = os.path.join(PKG, "hbm_probe")
+
+
+def build_hbm_probe() -> str:
+    """The HBM bandwidth probe (csrc/hbm_probe.hip, a measurement tool,
+    standalone)."""
+    cmd = [hipcc(), f"--offload-arch={ARCH}", "-O3", "-std=c++17", *DEVICE_FLAGS,
+           os.path.join(CSRC, "hbm_probe.hip"), "-o", HBM_PROBE]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"hbm probe build failed:\n{r.stdout}{r.stderr}")
+    return HBM_PROBE
+
+
 # Host-code sanitizers for the CPU tests of the C ABI: the host side
 # (ditmi.cpp: validation, workspace layout, tile planning, launch sequencing)
 # is rebuilt with AddressSanitizer and UndefinedBehaviorSanitizer; the kernel
