@@ -24,7 +24,8 @@
  * Conventions for every entry point:
  *   - Pointers to tensors are DEVICE pointers, 16-byte aligned, owned by the
  *     caller; the library never allocates or frees device memory while
- *     computing and keeps no device state.
+ *     computing.  Its only device state is the static scratch array of
+ *     dit_block_forward_noalloc (below), which lives until the process ends.
  *   - Weight matrices are row-major [out, in]; weights and biases have the
  *     element type shape.dtype (fp32 or bf16).  Residual streams, the
  *     conditioning vector, patches and outputs are always fp32.
