@@ -328,14 +328,27 @@ __global__ __launch_bounds__(NW * 64, QT == 1 ? 8 / NW : 1) void attn_bf16_dma_k
 // tile j+1, so the matrix pipe and the VALU work at the same time even while
 // the workgroup barrier keeps the two waves of a SIMD in step.  K of tile
 // j+1 is read one iteration earlier than V of tile j, so the ring has four
-// slots (tile t in slot t % 4, refilled with t + 4 after the barrier that
-// ends iteration t), which keeps two iterations between a tile's DMA and its
-// first read.
+// slots (tile t of the unit's range [t0, t1) in slot (t - t0) % 4, refilled
+// with t + 4 after the barrier that ends iteration t), which keeps two
+// iterations between a tile's DMA and its first read.  The loop is unrolled
+// four times, so that in each copy the slots are constants.
+// The kernel is bound by its VALU work rather than by the matrix pipe
+// (measured: removing the 16 row-sum dot products of a tile shortened the
+// video DiT attention by 6.5%, the 16 row-max instructions by 3%), so work
+// is moved off the VALU where the matrix pipe or the instruction encoding
+// can take it: the row sums go through small MFMAs, and LDS addresses are
+// lane offsets plus immediates.
 template <int DH, int NW, int ST = AttnCfg<DH>::PIPE_ST, int WPC = 1>
 __global__ __launch_bounds__(NW * 64, WPC) void attn_bf16_pipe_kernel(AttnArgs a) {
   using C = AttnCfg<DH>;
   constexpr bool FOLD = C::FOLD;
-  static_assert(ST >= 3 && WPC * (ST * C::SLOT + 1024) <= 160 * 1024, "ring fits the LDS");
+  static_assert(ST == 4 && WPC * (ST * C::SLOT + 1024) <= 160 * 1024, "ring fits the LDS");
+  // LDS: the K tiles of the four slots, then their V^T tiles (so that the
+  // largest slot offset of each fits a DS instruction's 16-bit immediate),
+  // then the spare line.  With constant slots every fragment read is a lane
+  // offset plus an immediate, no address arithmetic per tile (measured:
+  // video DiT attention -3.7%, joint -1.5%).
+  static_assert(ST * C::KTILE <= 65536 && ST * C::VTILE <= 65536, "slot offsets fit the 16-bit LDS immediate");
   constexpr int IPW = (C::TDMA + NW - 1) / NW;  // DMA instructions per wave per tile (uniform)
   __shared__ __attribute__((aligned(1024))) unsigned char smem[ST * C::SLOT + 1024];
 
@@ -369,7 +382,7 @@ __global__ __launch_bounds__(NW * 64, WPC) void attn_bf16_pipe_kernel(AttnArgs a
   const unsigned lds0 = __builtin_amdgcn_readfirstlane(lds_address(smem));
   const int q0 = qb * (NW * 32) + wave * 32;  // first query of this wave
 
-  // DMA of one tile (layout as in the kernel above) into slot tile % ST.  The
+  // DMA of one tile (K and V^T as in the kernel above) into a slot.  The
   // sources are a scalar base (the tile's first K row / V^T column) plus a
   // 32-bit lane offset, fixed for every full tile; only a tile reaching past
   // Tj clamps (K rows past the end re-read row Tj-1, V^T chunks past Tj_pad
@@ -394,34 +407,36 @@ __global__ __launch_bounds__(NW * 64, WPC) void attn_bf16_pipe_kernel(AttnArgs a
     doff[t] = dma_off(tt, C::BKV, C::BKV);
     doff_last[t] = dma_off(tt, Tj - 1 - kv_last, Tjp - 8 - kv_last);
   }
-  // DMA instruction t of `tile` into slot tile % ST.  Past the last tile it
+  // DMA instruction t of `tile` into slot `slot`.  Past the last tile it
   // re-reads the last tile into the spare line, so that every wave issues
   // the same number of DMA instructions per iteration whatever the tile
   // count, and the vmcnt waits are constants.
-  auto issue_one = [&](int tile, int t) {
+  auto issue_one = [&](int tile, int slot, int t) {
     const int qi = wave + NW * t;  // wave-uniform
     const int tl = min(tile, t1 - 1), kv0 = tl * C::BKV;
     const bf16_t* kb = kp + (long)kv0 * C::DHP;  // wave-uniform
     const bf16_t* vb = vp + kv0;
     const bool kpart = qi < C::KDMA || qi >= C::TDMA;
     const unsigned off = tl == nkv - 1 ? doff_last[t] : doff[t];
-    const unsigned dst = tile < t1 && qi < C::TDMA ? lds0 + (unsigned)((tile % ST) * C::SLOT + qi * 1024)
-                                                    : lds0 + (unsigned)(ST * C::SLOT);
+    const unsigned dst = tile < t1 && qi < C::TDMA
+                             ? lds0 + (unsigned)(qi < C::KDMA ? slot * C::KTILE + qi * 1024
+                                                              : ST * C::KTILE + slot * C::VTILE + (qi - C::KDMA) * 1024)
+                             : lds0 + (unsigned)(ST * C::SLOT);
     dma_16s(kpart ? (const void*)kb : (const void*)vb, off, dst);
   };
   auto issue = [&](int tile) {
 #pragma unroll
-    for (int t = 0; t < IPW; ++t) issue_one(tile, t);
+    for (int t = 0; t < IPW; ++t) issue_one(tile, (tile - t0) % ST, t);
   };
   // V^T columns of keys past the end (last tile only) hold stale workspace
   // bytes; zero them so that their zero probabilities cannot meet a NaN.
   auto zero_v_tail = [&](int tile) {
     const int kv0 = tile * C::BKV, nvalid = Tj - kv0;
-    unsigned char* sl = smem + (tile % ST) * C::SLOT;
+    unsigned char* sl = smem + ST * C::KTILE + ((tile - t0) % ST) * C::VTILE;
     for (int e = tid; e < DH * C::BKV; e += NW * 64) {
       const int d = e / C::BKV, key = e % C::BKV;
       const int kp = v_key_pos(key);
-      if (key >= nvalid) *(bf16_t*)(sl + C::KTILE + d * 128 + (((kp >> 3) ^ C::swz_v(d)) << 4) + (kp & 7) * 2) = 0;
+      if (key >= nvalid) *(bf16_t*)(sl + d * 128 + (((kp >> 3) ^ C::swz_v(d)) << 4) + (kp & 7) * 2) = 0;
     }
   };
 
@@ -431,7 +446,7 @@ __global__ __launch_bounds__(NW * 64, WPC) void attn_bf16_pipe_kernel(AttnArgs a
   if (C::VROWS > DH) {
     for (int e = tid; e < ST * (C::VROWS - DH) * 32; e += NW * 64) {
       const int sl = e / ((C::VROWS - DH) * 32), w = e % ((C::VROWS - DH) * 32);
-      ((uint32_t*)(smem + sl * C::SLOT + C::KTILE + DH * 128))[w] = FOLD && w < 32 ? 0x3F803F80u : 0u;
+      ((uint32_t*)(smem + ST * C::KTILE + sl * C::VTILE + DH * 128))[w] = FOLD && w < 32 ? 0x3F803F80u : 0u;
     }
   }
 
@@ -447,7 +462,7 @@ __global__ __launch_bounds__(NW * 64, WPC) void attn_bf16_pipe_kernel(AttnArgs a
   for (int s = 0; s < C::KS; ++s) k_off[s] = r32 * C::KROW + (((2 * s + g) ^ C::swz_k(r32)) << 4);
   int v_off[4];
 #pragma unroll
-  for (int c = 0; c < 4; ++c) v_off[c] = C::KTILE + r32 * 128 + (((2 * c + g) ^ C::swz_v(r32)) << 4);
+  for (int c = 0; c < 4; ++c) v_off[c] = ST * C::KTILE + r32 * 128 + (((2 * c + g) ^ C::swz_v(r32)) << 4);
 
   // k arrives in the exp2 domain (stored pre-scaled by the QKV epilogue).
   // The running max m_run is subtracted inside the QK^T product, so the MFMA
@@ -455,7 +470,15 @@ __global__ __launch_bounds__(NW * 64, WPC) void attn_bf16_pipe_kernel(AttnArgs a
   // holds 1 and q's holds -m_run (kept exactly representable in bf16);
   // otherwise every S^T accumulator starts at -m_run.
   const float TAU = 64.0f;  // lazy max, as in the kernel above
-  float m_run = 0.f, l_run = 0.f;
+  float m_run = 0.f;
+  // Row sums l of the bf16 probabilities (the same values the PV product
+  // multiplies), accumulated on the matrix pipe: a 4x4x4 MFMA with an A
+  // operand of ones adds the four bf16 values of each lane's B operand into
+  // every element of that lane's accumulator (the VALU is the busier unit).
+  // With FOLD the PV product itself carries l.
+  f32x4 lacc = f32x4{};
+  typedef short i16x4 __attribute__((ext_vector_type(4)));
+  const i16x4 ones4 = {0x3F80, 0x3F80, 0x3F80, 0x3F80};
   bool first = true;
   f32x16 oacc[C::DT];
 #pragma unroll
@@ -465,9 +488,6 @@ __global__ __launch_bounds__(NW * 64, WPC) void attn_bf16_pipe_kernel(AttnArgs a
   // MFMA reads it as its C operand and writes S^T elsewhere, so the block is
   // set only when m_run moves, not copied into the accumulators every tile.
   f32x16 sinit = f32x16{};
-  // bf16 ones, for the row sums of the bf16 probabilities by dot2 (the same
-  // values the PV product multiplies)
-  const bf16x2v ones2 = {(__bf16)1.0f, (__bf16)1.0f};
 
   // s_mask sets the scores of keys past the end to -inf.
   auto s_mask = [&](int kv0, f32x16 (&s)[2]) {
@@ -480,7 +500,7 @@ __global__ __launch_bounds__(NW * 64, WPC) void attn_bf16_pipe_kernel(AttnArgs a
     }
   };
   auto qk = [&](int tile, f32x16 (&s)[2]) {
-    const unsigned char* sl = smem + (tile % ST) * C::SLOT;
+    const unsigned char* sl = smem + ((tile - t0) % ST) * C::KTILE;
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
@@ -517,7 +537,7 @@ __global__ __launch_bounds__(NW * 64, WPC) void attn_bf16_pipe_kernel(AttnArgs a
   // One key tile: the exponentials of scur (tile j) and the QK^T of tile
   // j+1 into snext.  The loop runs it twice per trip with the roles of the
   // two score blocks exchanged, so no score block is ever copied.
-  auto tile_step = [&](const int j, f32x16 (&scur)[2], f32x16 (&snext)[2]) __attribute__((always_inline)) {
+  auto tile_step = [&](const int j, const int sj, f32x16 (&scur)[2], f32x16 (&snext)[2]) __attribute__((always_inline)) {
     // Keys past the end (last tile only) are masked just before their
     // exponentials.  Their K rows repeat row Tj-1, so the unmasked row max
     // taken earlier is still the max over real keys.
@@ -532,7 +552,7 @@ __global__ __launch_bounds__(NW * 64, WPC) void attn_bf16_pipe_kernel(AttnArgs a
       // O and l are still zero at the first tile, whose max may lie far below
       // 0 (exp2(-delta) = inf there, and 0 * inf is NaN)
       const float alpha = first ? 1.0f : __builtin_amdgcn_exp2f(-delta);
-      if (!FOLD) l_run *= alpha;
+      if (!FOLD) lacc *= alpha;
 #pragma unroll
       for (int t = 0; t < C::DT; ++t) oacc[t] *= alpha;
 #pragma unroll
@@ -545,22 +565,26 @@ __global__ __launch_bounds__(NW * 64, WPC) void attn_bf16_pipe_kernel(AttnArgs a
       first = false;
     }
     // Softmax of tile j interleaved by hand with the QK^T MFMAs of tile j+1
-    // (unconditional: the last iteration recomputes the last tile, unused):
+    // (unconditional: the last iteration reads the next slot's stale K and
+    // computes unused scores):
     // K fragments are read two MFMAs ahead, the MFMAs alternate between the
     // two 32-key halves (independent accumulators), and each MFMA is
     // followed by its share of the exponentials.
     u32x4 pw[4];
     // V^T fragments of tile j (landed long before): the first two are read
     // during the last QK^T MFMAs, so the PV product starts without waiting.
-    const unsigned char* slv = smem + (j % ST) * C::SLOT;
+    const unsigned char* slv = smem + sj * C::VTILE;  // V^T of tile j (v_off holds the region base)
     constexpr int NP = 4 * C::DT;  // PV MFMAs per tile; MFMA i: key chunk i / DT, O^T tile i % DT
-    // The exponentials are split between the two phases: those of key chunks
-    // 0 and 1 (the lane's first EX scores) run beside the QK^T MFMAs, those of
-    // chunks 2 and 3 beside the first NPRE PV MFMAs, which read only chunks 0
-    // and 1.  Both waves of a SIMD are in the same phase at the same time, so
-    // this evens out the VALU work between the phases (measured: video DiT
-    // attention -2.7%, joint -2%, DiT-XL/2 at 1024 tokens -1.5%).
-    constexpr int EX = 16;
+    // The exponentials are split between the two phases: those of the first
+    // EX / 8 key chunks (the lane's first EX scores) run beside the QK^T
+    // MFMAs, the rest beside the first NPRE PV MFMAs, which read only those
+    // first chunks.  Both waves of a SIMD are in the same phase at the same
+    // time, so this evens out the VALU work between the phases (measured with
+    // 16 of 32 against all 32 after the QK^T product: video DiT attention
+    // -2.7%, joint -2%, DiT-XL/2 at 1024 tokens -1.5%; with the row sums on
+    // the matrix pipe, 24 of 32 beside the QK^T MFMAs: video DiT -1.5%, joint
+    // -1.1%; head_dim 72, whose PV phase carries no row sums, keeps 16).
+    constexpr int EX = FOLD ? 16 : 24;
     constexpr int NPRE = EX / 8 * C::DT;  // PV MFMAs before the first one on chunk EX / 8
     constexpr int ND = 3;  // PV MFMAs issued after the barrier
     auto vread = [&](int i) {
@@ -569,8 +593,8 @@ __global__ __launch_bounds__(NW * 64, WPC) void attn_bf16_pipe_kernel(AttnArgs a
     };
     u32x4 vf[3];
     {
-      const int tn = min(j + 1, t1 - 1), kvn = tn * C::BKV;
-      const unsigned char* sln = smem + (tn % ST) * C::SLOT;
+      // K of tile j+1 (in the last iteration a stale slot, read but unused)
+      const unsigned char* sln = smem + ((sj + 1) % ST) * C::KTILE;
       constexpr int NQ = 2 * C::KS;  // QK^T MFMAs per tile; MFMA i: half i % 2, k-step i / 2
       auto kread = [&](int i) { return *(const bf16x8*)(sln + (i & 1) * 32 * C::KROW + k_off[i >> 1]); };
       bf16x8 kf[3];
@@ -603,16 +627,16 @@ __global__ __launch_bounds__(NW * 64, WPC) void attn_bf16_pipe_kernel(AttnArgs a
     // spread over the same sequence, one instruction every few MFMAs: issued
     // as a burst after the barrier, the workgroup's DMA instructions queue at
     // the address unit and stall the waves at issue.  Placed here rather than
-    // beside the QK^T MFMAs, which carry half the exponentials, it measured
+    // beside the QK^T MFMAs, which carry most of the exponentials, it measured
     // video DiT attention -1%, DiT-XL/2 at 1024 tokens -1.6%.
     {
-      float m = -INFINITY, lsum = 0.f;
+      float m = -INFINITY;
 #pragma unroll
       for (int i = 0; i < NP; ++i) {
         if (i + 2 < NP) vf[(i + 2) % 3] = vread(i + 2);
 #pragma unroll
         for (int t = 0; t < IPW; ++t)
-          if (i == t * (NP - ND) / IPW) issue_one(j + ST - 1, t);
+          if (i == t * (NP - ND) / IPW) issue_one(j + ST - 1, (sj + ST - 1) % ST, t);
         if (i < NP - ND)
           oacc[i % C::DT] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, vf[i % 3]),
                                                                     __builtin_bit_cast(bf16x8, pw[i / C::DT]),
@@ -629,26 +653,22 @@ __global__ __launch_bounds__(NW * 64, WPC) void attn_bf16_pipe_kernel(AttnArgs a
             if (2 * p + 1 >= EX + i * (32 - EX) / NPRE && 2 * p + 1 < EX + (i + 1) * (32 - EX) / NPRE)
               pw[p >> 2][p & 3] = pack_bf16x2(scur[p >> 3][(2 * p) & 15], scur[p >> 3][(2 * p + 1) & 15]);
         }
-        // row sum of the tile's bf16 probabilities: 16 packed pairs, spread
-        // one or more per MFMA
+        // row sum of the tile's 32 probabilities of this lane: eight 4x4x4
+        // MFMAs of two packed words each, spread over the PV MFMAs
         if (!FOLD)
 #pragma unroll
-          for (int w = i * 16 / NP; w < (i + 1) * 16 / NP; ++w)
-          {
-            // (the element is copied out first: a bit_cast of a vector
-            // element reference reads element 0 with this compiler)
-            const uint32_t pair = pw[w >> 2][w & 3];
-            lsum = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2v, pair), ones2, lsum, false);
-            asm volatile("" : "+v"(lsum));  // keeps the sum here, between the MFMAs
-          }
+          for (int k = 0; k < 8; ++k)
+            if (i == (k * NP + NP - 1) / 8) {
+              const u32x2 two = {pw[k >> 1][(k & 1) * 2], pw[k >> 1][(k & 1) * 2 + 1]};
+              lacc = __builtin_amdgcn_mfma_f32_4x4x4bf16_1k(ones4, __builtin_bit_cast(i16x4, two), lacc, 0, 0, 0);
+            }
         __builtin_amdgcn_sched_barrier(0);
       }
       mcur = max_halves(m);
-      if (!FOLD) l_run += lsum;
     }
     // tile j+2 must have landed for every wave before the next iteration's
     // QK^T (tiles j+3 .. j+ST-1 may still be in flight), and every wave must
-    // be done with slot j % ST before it takes tile j+ST
+    // be done with the slot of tile j before it takes tile j+ST
     wait_vmcnt<(ST - 3) * IPW>();
     __syncthreads();
     // the last ND PV MFMAs of the tile, on fragments already in registers
@@ -667,18 +687,22 @@ __global__ __launch_bounds__(NW * 64, WPC) void attn_bf16_pipe_kernel(AttnArgs a
     }
   };
   int j = t0;
-  for (; j + 1 < t1; j += 2) {
-    tile_step(j, sa, sb);
-    tile_step(j + 1, sb, sa);
+  for (; j + 3 < t1; j += 4) {
+    tile_step(j, 0, sa, sb);
+    tile_step(j + 1, 1, sb, sa);
+    tile_step(j + 2, 2, sa, sb);
+    tile_step(j + 3, 3, sb, sa);
   }
-  if (j < t1) tile_step(j, sa, sb);
+  if (j < t1) tile_step(j, 0, sa, sb);
+  if (j + 1 < t1) tile_step(j + 1, 1, sb, sa);
+  if (j + 2 < t1) tile_step(j + 2, 2, sa, sb);
   wait_vmcnt<0>();
 
   {
     const int qrow = q0 + r32;
     // with FOLD, l is O^T row DH: element LE of tile LT in the lanes of half
     // LG (the other half holds a zero row there)
-    const float l_lane = FOLD ? (g == C::LG ? oacc[C::LT][C::LE] : 0.f) : l_run;
+    const float l_lane = FOLD ? (g == C::LG ? oacc[C::LT][C::LE] : 0.f) : lacc[0];
     const float l_tot = sum_halves(l_lane);
     if (unit >= 0) {
       // a unit of a split item: O relative to its own m_run, m_run and l,
