@@ -108,6 +108,13 @@ SMALL = [
     ("bf16_pipe_dh72_t150_b16", synth.CONFIGS["c1"].with_(batch=16, tokens=150, n_blocks=1)),
     ("bf16_pipe_joint_dh128", synth.CONFIGS["c3"].with_(batch=32, tokens=120, text_tokens=9, hidden=1024, heads=8,
                                                         head_dim=128, mlp_hidden=512, n_blocks=1)),
+    # the key loop runs four tiles per trip (one per ring slot): five, eight
+    # and seven key tiles leave one, none and three tiles after the trips
+    ("bf16_pipe_dh128_t300_b16", synth.CONFIGS["c1"].with_(batch=16, tokens=300, hidden=1024, heads=8, head_dim=128,
+                                                           mlp_hidden=512, n_blocks=1)),
+    ("bf16_pipe_dh72_t450_b8", synth.CONFIGS["c1"].with_(batch=8, tokens=450, n_blocks=1)),
+    ("bf16_pipe_dh64_t420_b16", synth.CONFIGS["c1"].with_(batch=16, tokens=420, hidden=1024, heads=16, head_dim=64,
+                                                          mlp_hidden=512, n_blocks=1)),
 ]
 
 
