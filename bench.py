@@ -295,6 +295,9 @@ def summarize_profile(key, trace_dir, pmc_dir, fetch_dir, write_dir, bench_json,
 
 class Workload:
     def __init__(self, cfg, torch, dm):
+        if cfg.grid is not None and cfg.grid[0] * cfg.grid[1] != cfg.tokens:
+            # the step reads one position row per token
+            raise ValueError(f"{cfg.name}: position grid {cfg.grid} does not match {cfg.tokens} tokens")
         self.cfg = cfg
         self.torch = torch
         self.dm = dm

@@ -179,6 +179,17 @@ class StepWeightTable:
         self._keep = (step_w, blocks, pos)
 
 
+def _check_pos(shape: Shape, pos: Optional[torch.Tensor]) -> None:
+    """The step reads the position table as [tokens, hidden] fp32 rows; the C
+    ABI cannot see the size of a device buffer, so a short table is refused
+    here rather than read past its end on the device."""
+    if pos is None:
+        return
+    if pos.dim() != 2 or pos.shape[0] < shape.tokens or pos.shape[1] != shape.hidden:
+        raise ValueError(f"pos is {tuple(pos.shape)}; the step reads [{shape.tokens}, {shape.hidden}] "
+                         "(one row per image token)")
+
+
 # ---------------------------------------------------------------- entry points
 def workspace_bytes(shape: Shape, kind: int = DIT_WS_BLOCK) -> int:
     n = lib().dit_workspace_bytes(ctypes.byref(shape), kind)
@@ -212,6 +223,7 @@ def block_forward_noalloc(shape: Shape, weights: BlockWeights, x: torch.Tensor, 
 def step_forward(shape: Shape, table: StepWeightTable, patches: torch.Tensor, cond: torch.Tensor, out: torch.Tensor,
                  workspace: torch.Tensor, x_txt: Optional[torch.Tensor] = None, stream=None) -> None:
     """One denoising step (patch embed, blocks, final layer) into out."""
+    _check_pos(shape, table._keep[2])
     _check(lib().dit_step_forward(ctypes.byref(shape), ctypes.byref(table.struct),
                                   _ptr(patches, torch.float32, "patches"), _ptr(x_txt, torch.float32, "x_txt"),
                                   _ptr(cond, torch.float32, "cond"), _ptr(out, torch.float32, "out"),
@@ -226,6 +238,7 @@ def sample_euler(shape: Shape, table: StepWeightTable, z: torch.Tensor, sigmas, 
     """Multi-step Euler loop over the step (z updated in place): with cond_w and
     y the conditioning is recomputed per step at t_i = sigmas[i] * t_scale;
     otherwise cond is used for every step.  sigmas: n_steps + 1 floats (host)."""
+    _check_pos(shape, table._keep[2])
     sig = [float(v) for v in sigmas]
     if len(sig) < 1:
         raise ValueError("sigmas needs at least one value")
@@ -257,6 +270,7 @@ def serve(shape: Shape, table: StepWeightTable, requests, sigmas, workspace: tor
     list of dicts with host tensors z_in, z_out ([B,T,P] fp32, ideally pinned)
     and y ([B] int32, with cond_w) or cond ([B,D] fp32).  Returns after
     enqueueing; synchronise the stream before reading z_out."""
+    _check_pos(shape, table._keep[2])
     sig = [float(v) for v in sigmas]
     arr = (ctypes.c_float * len(sig))(*sig)
     reqs = (Request * max(1, len(requests)))()

@@ -1,6 +1,6 @@
-"""Host-side logic of bench.py (CPU): the one-GPU contract, the algorithmic
-flop count behind the step TFLOP/s, and the source-hash gate on the
-committed HBM traffic records."""
+"""Host-side logic of bench.py and the binding (CPU): the one-GPU contract,
+the algorithmic flop count behind the step TFLOP/s, the source-hash gate on
+the committed HBM traffic records, and the position-table size check."""
 import json
 import os
 import subprocess
@@ -51,3 +51,22 @@ def test_traffic_record_only_for_the_current_source(tmp_path, monkeypatch):
     (tmp_path / "attention_w_traffic.json").write_text(json.dumps(rec))
     assert bench.traffic_from_profile("attention", "w") is None
     assert bench.traffic_from_profile("attention", "absent") is None
+
+
+def test_position_table_must_cover_the_tokens():
+    """A position table shorter than the token count would be read past its
+    end by the patch embedding on the device; the binding and the bench
+    refuse it on the host."""
+    import torch
+    import synth
+    import paper_2605_25550_amd as dm
+    cfg = synth.CONFIGS["c2"]
+    shape = dm.shape_of(cfg)
+    dm._check_pos(shape, None)
+    dm._check_pos(shape, torch.zeros(cfg.tokens, cfg.hidden))
+    for bad in (torch.zeros(cfg.tokens - 1, cfg.hidden), torch.zeros(cfg.tokens, cfg.hidden + 1),
+                torch.zeros(cfg.tokens * cfg.hidden)):
+        with pytest.raises(ValueError):
+            dm._check_pos(shape, bad)
+    with pytest.raises(ValueError):
+        bench.Workload(cfg.with_(tokens=2 * cfg.tokens), torch, dm)
