@@ -727,14 +727,35 @@ __global__ __launch_bounds__(NW * 64, WPC) void attn_bf16_pipe_kernel(AttnArgs a
       const long orow = qrow < a.T_img ? (long)b * a.T_img + qrow
                                        : (long)a.B * a.T_img + (long)b * a.T_txt + (qrow - a.T_img);
       bf16_t* op = (bf16_t*)a.o + orow * a.D + h * DH;
+      // Lane half g holds columns 8 jj + 4 g .. +3 of each O^T tile.  For a
+      // pair of 8-column groups (jj, jj+1) a swap between the halves gives
+      // half 0 columns 0..7 of the pair and half 1 columns 8..15, so each
+      // lane stores 16 contiguous bytes and a row's 32 bytes come from one
+      // instruction.
 #pragma unroll
       for (int t = 0; t < C::DT; ++t)
 #pragma unroll
-        for (int jj = 0; jj < 4; ++jj) {
-          const int d = t * 32 + jj * 8 + g * 4;
-          if (d < DH)
-            *(u32x2*)(op + d) = u32x2{pack_bf16x2(oacc[t][jj * 4 + 0] * inv, oacc[t][jj * 4 + 1] * inv),
-                                      pack_bf16x2(oacc[t][jj * 4 + 2] * inv, oacc[t][jj * 4 + 3] * inv)};
+        for (int jp = 0; jp < 2; ++jp) {
+          const int d0 = t * 32 + jp * 16;
+          auto word = [&](int jj, int k) {
+            return pack_bf16x2(oacc[t][jj * 4 + 2 * k] * inv, oacc[t][jj * 4 + 2 * k + 1] * inv);
+          };
+          if (d0 + 16 <= DH) {
+            u32x4 w;
+#pragma unroll
+            for (int k = 0; k < 2; ++k) {
+              const auto r = __builtin_amdgcn_permlane32_swap(word(2 * jp, k), word(2 * jp + 1, k), false, false);
+              w[k] = r[0];
+              w[2 + k] = r[1];
+            }
+            *(u32x4*)(op + d0 + g * 8) = w;
+          } else {
+#pragma unroll
+            for (int jj = 2 * jp; jj < 2 * jp + 2; ++jj) {
+              const int d = t * 32 + jj * 8 + g * 4;
+              if (d < DH) *(u32x2*)(op + d) = u32x2{word(jj, 0), word(jj, 1)};
+            }
+          }
         }
     }
   }
