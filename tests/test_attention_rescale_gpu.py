@@ -11,8 +11,10 @@ zero; both cases are forced here:
   to the q projection (so a query scores highest against keys of its own
   direction) and both are scaled by a power of two, so queries after the
   boundary see a later tile lead the first tiles' max by about a hundred or
-  more (log2 units).  The boundary at 64 or 128 tokens puts the move in the
-  first or the second tile of the kernel's two-tile loop trip.
+  more (log2 units).  At 150 tokens the boundary at 64 or 128 tokens puts
+  the move in the second or third key tile; at 600 tokens, boundaries at
+  320 and 448 put it inside the second trip of the pipelined kernel's
+  four-tile loop (its second and fourth ring slot).
 - a first tile far below zero: the first tokens point the opposite way, so
   for queries after the boundary every score of the first tile is below
   -128, where the first max, taken as the new m_run, would overflow a
@@ -81,6 +83,12 @@ def _cfg(kind):
         "pipe_dh72_fold": synth.CONFIGS["c1"].with_(batch=16, tokens=150, n_blocks=1),
         "pipe_dh64": synth.CONFIGS["c1"].with_(batch=16, tokens=150, hidden=1024, heads=16, head_dim=64,
                                                mlp_hidden=512, n_blocks=1),
+        # ten key tiles: two four-tile trips of the pipelined kernel's loop and two after them
+        "pipe_dh128_long": synth.CONFIGS["c1"].with_(batch=12, tokens=600, hidden=1024, heads=8, head_dim=128,
+                                                     mlp_hidden=512, n_blocks=1),
+        "pipe_dh72_fold_long": synth.CONFIGS["c1"].with_(batch=6, tokens=600, n_blocks=1),
+        "pipe_dh64_long": synth.CONFIGS["c1"].with_(batch=6, tokens=600, hidden=1024, heads=16, head_dim=64,
+                                                    mlp_hidden=512, n_blocks=1),
         # small grids: the four-wave kernel
         "small_dh128": synth.CONFIGS["c1"].with_(batch=2, tokens=150, hidden=256, heads=2, head_dim=128,
                                                  mlp_hidden=512, n_blocks=1),
@@ -95,6 +103,15 @@ MOVE = [("pipe_dh128", 4.0), ("pipe_dh72_fold", 4.0), ("pipe_dh64", 8.0), ("smal
 # (case, q/k scale, amplitude): first tiles far below zero for some later queries
 LOW = [("pipe_dh128", 4.0, 20.0), ("pipe_dh72_fold", 4.0, 20.0), ("pipe_dh64", 8.0, 6.0),
        ("small_dh72_fold", 8.0, 6.0)]
+
+
+MOVE_LONG = [("pipe_dh128_long", 4.0), ("pipe_dh72_fold_long", 4.0), ("pipe_dh64_long", 8.0)]
+
+
+@pytest.mark.parametrize("boundary", [320, 448])
+@pytest.mark.parametrize("name,scale", MOVE_LONG, ids=[m[0] for m in MOVE_LONG])
+def test_lazy_max_moves_inside_a_loop_trip(name, scale, boundary):
+    test_lazy_max_moves_mid_sequence(name, scale, boundary)
 
 
 @pytest.mark.parametrize("boundary", [64, 128])
